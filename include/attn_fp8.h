@@ -1,0 +1,137 @@
+/*
+ * attn_fp8.h -- C ABI of libattn_fp8.so: FP8 online-softmax attention forward
+ * for AMD Instinct MI355X (gfx950), with a static P-scale S and a runtime
+ * KV-block iteration order.
+ *
+ * The operation is Algorithm 1 of "P-Cast Precision in FP8 Attention:
+ * Sink-Induced Collapse and the Optimality of S = 2^8" (Sec. 2.2), applied to
+ * every query row of every (batch, head), with the kernel semantics of
+ * Sec. 6.1:
+ *   for each KV block j in the chosen order:
+ *     Z     = Q K_j^T / sqrt(d)                        (FP32 scores)
+ *     m_new = max(m, max Z);  alpha = exp(m - m_new)
+ *     P     = exp(Z - m_new)                           (FP32)
+ *     l     = alpha * l + sum(P)                       (pre-cast P)
+ *     P8    = cast_E4M3(P * S)                         (round to nearest even)
+ *     O     = alpha * O + P8 . V_j                     (FP32 accumulator)
+ *   out = O / (S * l)
+ * Base-2 form used on the device: with c = fl32(log2(e)/sqrt(d)) and D the
+ * raw dot product q.k, mc = fl(m*c), x = fma(D, c, -mc), P = exp2(x),
+ * alpha = exp2(mc_old - mc_new).  KV blocks are [j*block_kv, (j+1)*block_kv)
+ * anchored at key 0; ORDER_FORWARD visits j = 0, 1, ...; ORDER_REVERSE visits
+ * the last block first and the sink block (block 0) last (Sec. 4.1).  Under
+ * causal masking, row r sees keys t <= r only and visits only the blocks that
+ * hold at least one such key; masked keys take no part in l, O or the counts.
+ * The running maximum is updated once per KV block, never lazily.
+ *
+ * Memory layout (all contiguous, row-major, device memory owned by the caller):
+ *   q    [B][Hq][N][d]
+ *   k, v [B][Hkv][N][d]      (query head h reads KV head h / (Hq/Hkv))
+ *   out  [B][Hq][N][d]  float32
+ *   lse  [B][Hq][N]     float32, natural-log log-sum-exp of z = q.k/sqrt(d)
+ *                               over the row's valid keys (independent of S)
+ *   counts [B][Hq][N][3] uint32 (p_underflow_count only)
+ *
+ * Element types by mode:
+ *   ATTN_MODE_FAITHFUL : q, k, v float32.  Scores and P.V on FP32 MFMA; exp2
+ *                        evaluated in FP64 and rounded to FP32; P*S rounded to
+ *                        E4M3 by the hardware convert and decoded back to FP32
+ *                        (Sec. 6.1: Q, K, V kept in FP32 to isolate the cast).
+ *   ATTN_MODE_FAST     : q, k bfloat16 (raw 16-bit patterns), v OCP E4M3 bytes.
+ *                        Scores on the bf16 MFMA, exp2 by the hardware
+ *                        instruction, E4M3 P bytes straight into the FP8 MFMA.
+ *   ATTN_MODE_NOCAST   : like FAITHFUL with the cast disabled (P*S used as is);
+ *                        a diagnostic for the FP64 comparison.
+ *   The E4M3 cast saturates: P*S >= 448 becomes 448 (reachable only for S > 448).
+ *
+ * Ownership and threading: every pointer is a device pointer owned by the
+ * caller.  The library allocates no memory, keeps no per-call state, and is
+ * reentrant.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ * stream) and runs asynchronously: a return of ATTN_OK means "validated and
+ * launched"; synchronise on the stream before reading results.
+ *
+ * Errors: arguments are validated before any HIP call; on failure nothing is
+ * launched and the return value says why.  A launch failure reported by the
+ * HIP runtime returns ATTN_ERR_HIP.  No C++ exception crosses this interface.
+ */
+#ifndef ATTN_FP8_H
+#define ATTN_FP8_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    ATTN_MODE_FAITHFUL = 0,
+    ATTN_MODE_FAST = 1,
+    ATTN_MODE_NOCAST = 2
+};
+
+enum {
+    ATTN_ORDER_FORWARD = 0, /* KV blocks 0, 1, ..., last (sink block first)  */
+    ATTN_ORDER_REVERSE = 1  /* KV blocks last, ..., 1, 0 (sink block last)   */
+};
+
+enum {
+    ATTN_OK = 0,
+    ATTN_ERR_INVALID_ARG = -1, /* null pointer, bad shape, S not finite/positive, ... */
+    ATTN_ERR_UNSUPPORTED = -2, /* valid but not built: d or block_kv outside {64,128} */
+    ATTN_ERR_HIP = -3          /* the HIP runtime rejected the launch */
+};
+
+/*
+ * Attention forward (Algorithm 1 over every row).
+ *   q, k, v   device inputs, element type by `mode` (see above).
+ *   out       device float32 [B][Hq][N][d]; required.
+ *   lse       device float32 [B][Hq][N]; may be NULL.
+ *   B, Hq, Hkv, N, d
+ *             batch, query heads, KV heads (Hq % Hkv == 0), sequence length,
+ *             head dimension (64 or 128).  N may be any value >= 0; B*Hq*N == 0
+ *             is a no-op (pointers are then not inspected).
+ *   causal    0 or 1.
+ *   block_kv  KV block size B of Algorithm 1: 64 or 128.  It is the granularity
+ *             of the running-maximum update and therefore part of the result.
+ *   order     ATTN_ORDER_FORWARD or ATTN_ORDER_REVERSE.
+ *   S         static P-scale (Sec. 5), finite and > 0.  Powers of two make the
+ *             scaling exact (Prop. 2); S = 256 is the paper's choice.
+ *   mode      ATTN_MODE_*.
+ *   stream    hipStream_t or NULL.
+ * Returns ATTN_OK or an ATTN_ERR_* code.
+ */
+int attn_fp8_fwd(const void* q, const void* k, const void* v, float* out,
+                 float* lse, int B, int Hq, int Hkv, int N, int d, int causal,
+                 int block_kv, int order, float S, int mode, void* stream);
+
+/*
+ * P-underflow diagnostic (Prop. 1): runs the same computation as attn_fp8_fwd
+ * and, for every query row, counts the valid keys whose cast code
+ * E4M3(P*S) is zero, split by key position:
+ *   counts[row][0]: keys t <  n_sink                 (the sink keys)
+ *   counts[row][1]: keys n_sink <= t < block_kv      (non-sink keys sharing
+ *                                                     the sink's KV block)
+ *   counts[row][2]: keys t >= block_kv               (all other blocks)
+ *   counts    device uint32 [B][Hq][N][3]; required; every entry is written.
+ *   n_sink    >= 0.
+ *   out, lse  optional (NULL allowed); when given they receive the same
+ *             values attn_fp8_fwd writes.
+ * Other arguments and return codes as for attn_fp8_fwd.
+ */
+int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v,
+                               int B, int Hq, int Hkv, int N, int d, int causal,
+                               int block_kv, int order, float S, int mode,
+                               int n_sink, uint32_t* counts, float* out,
+                               float* lse, void* stream);
+
+/* Static, human-readable text for a status code (never NULL). */
+const char* attn_fp8_strerror(int status);
+
+/* Library version: major*10000 + minor*100 + patch. */
+int attn_fp8_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ATTN_FP8_H */

@@ -1,0 +1,143 @@
+"""CPU oracle for FP8 online-softmax attention (test infrastructure).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product path (the HIP library and
+its binding) never touches it, and the two share no code.
+
+``liboracle.so`` is built from ``oracle.c`` with gcc (``build()``); the
+Python side only marshals numpy arrays.  ``analysis`` holds the closed forms of
+the paper (dp(S), F(Delta, S), delta_k).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+ORDER = {"forward": 0, "reverse": 1}
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+        cmd = ["gcc", "-O2", "-std=c11", "-fno-fast-math", "-ffp-contract=off",
+               "-fPIC", "-shared", "-pthread", "-o", tmp, _SRC, "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        L = ctypes.CDLL(_LIB_PATH)
+        P = ctypes.c_void_p
+        i32, i64, f32 = ctypes.c_int, ctypes.c_int64, ctypes.c_float
+        L.oracle_e4m3_encode.argtypes = [f32]
+        L.oracle_e4m3_encode.restype = ctypes.c_uint8
+        L.oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
+        L.oracle_e4m3_decode.restype = f32
+        L.oracle_e4m3_encode_array.argtypes = [P, P, i64]
+        L.oracle_e4m3_encode_array.restype = None
+        L.oracle_e4m3_decode_array.argtypes = [P, P, i64]
+        L.oracle_e4m3_decode_array.restype = None
+        L.oracle_attn.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, P, i64, i32]
+        L.oracle_attn.restype = i32
+        L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
+        L.oracle_ref_fp64.restype = i32
+        L.oracle_version.restype = i32
+        _lib = L
+    return _lib
+
+
+def default_threads() -> int:
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:  # pragma: no cover
+        return max(1, os.cpu_count() or 1)
+
+
+def _ptr(a: np.ndarray | None):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def e4m3_encode(x) -> np.ndarray:
+    """Bit-level OCP E4M3 encoding (RNE, subnormals, satfinite) of float32 data."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.float32))
+    out = np.empty(x.shape, dtype=np.uint8)
+    lib().oracle_e4m3_encode_array(_ptr(x), _ptr(out), x.size)
+    return out
+
+
+def e4m3_decode(codes) -> np.ndarray:
+    codes = np.ascontiguousarray(np.asarray(codes, dtype=np.uint8))
+    out = np.empty(codes.shape, dtype=np.float32)
+    lib().oracle_e4m3_decode_array(_ptr(codes), _ptr(out), codes.size)
+    return out
+
+
+def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
+         cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None):
+    """Algorithm 1 on the given rows.
+
+    q: [B,Hq,N,d]; k, v: [B,Hkv,N,d]; float32 arrays holding the exact values
+    the device consumed.  rows: flat row ids ((b*Hq+hq)*N + r) or None for all.
+    Returns (out [n_rows,d] float32, lse [n_rows] float32, counts [n_rows,3] uint32).
+    """
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    if rows is None:
+        n_rows = B * Hq * N
+        rows_a = None
+    else:
+        rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        n_rows = rows_a.size
+    out = np.empty((n_rows, d), dtype=np.float32)
+    lse = np.empty(n_rows, dtype=np.float32)
+    counts = np.zeros((n_rows, 3), dtype=np.uint32)
+    rc = lib().oracle_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                           B, Hq, Hkv, N, d, int(bool(causal)), int(block_kv),
+                           ORDER[order], float(S), int(bool(cast)), int(n_sink),
+                           _ptr(rows_a), n_rows, nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("oracle_attn rejected its arguments")
+    return out, lse, counts
+
+
+def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None = None):
+    """Textbook softmax attention in FP64 (no blocks, no cast) on the given rows.
+
+    Returns (out [n_rows,d] float64, lse [n_rows] float64).
+    """
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    if rows is None:
+        n_rows = B * Hq * N
+        rows_a = None
+    else:
+        rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        n_rows = rows_a.size
+    out = np.empty((n_rows, d), dtype=np.float64)
+    lse = np.empty(n_rows, dtype=np.float64)
+    rc = lib().oracle_ref_fp64(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                               B, Hq, Hkv, N, d, int(bool(causal)),
+                               _ptr(rows_a), n_rows, nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("oracle_ref_fp64 rejected its arguments")
+    return out, lse

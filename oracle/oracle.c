@@ -1,0 +1,418 @@
+/*
+ * CPU oracle for FP8 online-softmax attention with a static P-scale S and a
+ * runtime KV-block order.  TEST INFRASTRUCTURE ONLY: the product path never
+ * links, loads or calls this file; tests, the smoke check and the benchmark's
+ * CPU-baseline leg do.  It shares no code, header or table with the GPU
+ * library.
+ *
+ * Plain, slow and sequential per query row.  Threads only split the list of
+ * rows; every row is computed exactly as written below.
+ *
+ * What it follows in the paper:
+ *   - E4M3 number line (Sec. 2.1, the subnormal and normal equations and the
+ *     key-thresholds table): sign bit, 4 exponent bits with bias 7, 3 mantissa
+ *     bits, subnormals M/8 * 2^-6, normals 2^(E-7) (1 + M/8), E=15,M=7 is NaN,
+ *     max 448.
+ *   - Algorithm 1 (FP8 online softmax attention, one query row) together with
+ *     the kernel-faithful simulation rules of Sec. 6.1: l from the pre-cast
+ *     FP32 P, O from the cast P, round-to-nearest E4M3 cast of P*S, epilogue
+ *     O / (S * l).
+ *   - Prop. 1 (P-underflow condition): a P value underflows when its code is
+ *     zero; the diagnostic counts those codes per key category.
+ *
+ * Readings where the paper leaves the arithmetic open (each also listed in
+ * the design notes of the repository):
+ *   - scores use exp2 with c = log2(e)/sqrt(d) folded in, i.e.
+ *     exp(z - m) = exp2(D*c - m*c) with D the raw dot q.k;
+ *     mc = fl(m*c), x = fma(D, c, -mc), alpha = exp2(mc_old - mc_new);
+ *   - exp2 is evaluated in double and rounded once to float;
+ *   - the E4M3 cast is round-to-nearest-even, keeps subnormals, and saturates
+ *     to +-448 (NaN stays NaN), so 2^-10 itself rounds to zero;
+ *   - KV blocks are [j*Bc, (j+1)*Bc) anchored at key 0; reverse visits the
+ *     last block first; under causal masking a row visits only the blocks
+ *     holding at least one key t <= r, and masked keys take no part in l, O or
+ *     the counts.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_VERSION 1
+
+/* ------------------------------------------------------------------------- */
+/* OCP E4M3 (Sec. 2.1)                                                        */
+/* ------------------------------------------------------------------------- */
+
+/* Decode one E4M3 byte: subnormal (E=0) v = M/8 * 2^-6, normal
+ * v = 2^(E-7) * (1 + M/8); E=15, M=7 is NaN. */
+float oracle_e4m3_decode(uint8_t code)
+{
+    int sign = code >> 7;
+    int E = (code >> 3) & 0xF;
+    int M = code & 0x7;
+    float v;
+    if (E == 15 && M == 7)
+        return NAN;
+    if (E == 0)
+        v = ldexpf((float)M, -9);           /* (M/8) * 2^-6 */
+    else
+        v = ldexpf((float)(8 + M), E - 10); /* (1 + M/8) * 2^(E-7) */
+    return sign ? -v : v;
+}
+
+/* Encode one FP32 value to E4M3: round to nearest, ties to even code,
+ * subnormals kept, |y| >= 448 saturates to 448, NaN -> 0x7F | sign.
+ * Works on the FP32 bit pattern only. */
+uint8_t oracle_e4m3_encode(float y)
+{
+    uint32_t u;
+    memcpy(&u, &y, 4);
+    uint8_t sign = (uint8_t)((u >> 24) & 0x80);
+    uint32_t a = u & 0x7FFFFFFFu;
+    if (a > 0x7F800000u)               /* NaN */
+        return sign | 0x7F;
+    if (a >= 0x43E00000u)              /* |y| >= 448 (and inf): saturate */
+        return sign | 0x7E;
+    if (a == 0)
+        return sign;
+    int e = (int)(a >> 23) - 127;      /* unbiased exponent; a is normal or
+                                          FP32-subnormal (then e = -127) */
+    if (e >= -6) {
+        /* E4M3 normal binade [2^e, 2^(e+1)): keep 3 of the 23 mantissa bits,
+         * round the dropped 20 bits to nearest, ties to even. */
+        uint32_t mant = a & 0x7FFFFFu;
+        uint32_t keep = mant >> 20;
+        uint32_t rest = mant & 0xFFFFFu;
+        const uint32_t half = 0x80000u;
+        if (rest > half || (rest == half && (keep & 1u)))
+            keep++;
+        int E = e + 7;
+        if (keep == 8) {               /* mantissa carry into the exponent */
+            keep = 0;
+            E++;
+        }
+        return sign | (uint8_t)((E << 3) | keep);
+    }
+    /* Below the smallest normal 2^-6: the grid is uniform with step 2^-9, so
+     * the code is the integer nearest |y| * 2^9 (exact multiply), ties to
+     * even.  n == 8 is the smallest normal, code 0x08. */
+    {
+        float v = fabsf(y) * 512.0f;
+        uint32_t n = (uint32_t)v;      /* truncation; v < 8 */
+        float frac = v - (float)n;     /* exact */
+        if (frac > 0.5f || (frac == 0.5f && (n & 1u)))
+            n++;
+        return sign | (uint8_t)n;
+    }
+}
+
+void oracle_e4m3_encode_array(const float* x, uint8_t* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++)
+        out[i] = oracle_e4m3_encode(x[i]);
+}
+
+void oracle_e4m3_decode_array(const uint8_t* x, float* out, int64_t n)
+{
+    for (int64_t i = 0; i < n; i++)
+        out[i] = oracle_e4m3_decode(x[i]);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Algorithm 1, one query row                                                 */
+/* ------------------------------------------------------------------------- */
+
+enum { ORDER_FORWARD = 0, ORDER_REVERSE = 1 };
+enum { CAST_NONE = 0, CAST_E4M3 = 1 };
+
+typedef struct {
+    const float* q;     /* [B][Hq][N][d]  */
+    const float* k;     /* [B][Hkv][N][d] */
+    const float* v;     /* [B][Hkv][N][d] */
+    float* out;         /* [n_rows][d]    */
+    float* lse;         /* [n_rows]       (nullable) */
+    uint32_t* counts;   /* [n_rows][3]    (nullable) */
+    int B, Hq, Hkv, N, d, causal, Bc, order, cast, n_sink;
+    float S;
+    const int64_t* rows;/* flat (b*Hq + hq)*N + r, n_rows of them */
+    int64_t n_rows;
+    int nthreads;
+    int64_t next;       /* work counter */
+    pthread_mutex_t lock;
+} attn_job;
+
+static void attn_row(const attn_job* J, int64_t flat, float* out_row,
+                     float* lse_row, uint32_t* cnt_row, float* D, float* P,
+                     float* o, float* blk)
+{
+    const int N = J->N, d = J->d, Bc = J->Bc;
+    const int64_t bh = flat / N;
+    const int r = (int)(flat % N);
+    const int b = (int)(bh / J->Hq), hq = (int)(bh % J->Hq);
+    const int hk = hq / (J->Hq / J->Hkv);
+    const float* qr = J->q + flat * (int64_t)d;
+    const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
+    const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
+    const float S = J->S;
+    /* exp(z) with z = D/sqrt(d) is exp2(D * c); c rounded once from double */
+    const float c = (float)(1.4426950408889634074 / sqrt((double)d));
+
+    const int L = J->causal ? r + 1 : N;        /* valid keys 0..L-1 */
+    const int nblk = (L + Bc - 1) / Bc;
+
+    /* line: m <- -inf, l <- 0, O <- 0 (FP32) */
+    float m = -INFINITY, mc = -INFINITY, ell = 0.0f;
+    for (int i = 0; i < d; i++)
+        o[i] = 0.0f;
+    if (cnt_row)
+        cnt_row[0] = cnt_row[1] = cnt_row[2] = 0;
+
+    for (int it = 0; it < nblk; it++) {
+        /* BlockOrder: forward 0..nblk-1, reverse nblk-1..0 */
+        const int j = (J->order == ORDER_FORWARD) ? it : nblk - 1 - it;
+        const int t0 = j * Bc;
+        const int t1 = (t0 + Bc < L) ? t0 + Bc : L;
+        const int nt = t1 - t0;
+
+        /* scores: raw dot products, rounded once to FP32 */
+        float mloc = -INFINITY;
+        for (int t = 0; t < nt; t++) {
+            const float* kt = K + (int64_t)(t0 + t) * d;
+            double acc = 0.0;
+            for (int i = 0; i < d; i++)
+                acc += (double)qr[i] * (double)kt[i];
+            D[t] = (float)acc;
+            if (D[t] > mloc)
+                mloc = D[t];
+        }
+        /* m_new = max(m, m_loc); alpha = exp(m - m_new) in base 2 */
+        const float m_new = (m > mloc) ? m : mloc;
+        const float mc_new = m_new * c;
+        const float alpha = (float)exp2((double)(mc - mc_new));
+
+        /* P = exp(Z - m_new) in FP32, l <- alpha*l + sum(P) (pre-cast) */
+        float psum = 0.0f;
+        for (int t = 0; t < nt; t++) {
+            const float x = fmaf(D[t], c, -mc_new);
+            P[t] = (float)exp2((double)x);
+            psum += P[t];
+        }
+        ell = alpha * ell + psum;
+
+        /* P-cast: P_fp8 = cast_E4M3(P * S); the P-underflow diagnostic counts
+         * zero codes per key category */
+        for (int t = 0; t < nt; t++) {
+            const float y = P[t] * S;
+            if (J->cast == CAST_E4M3) {
+                const uint8_t e = oracle_e4m3_encode(y);
+                if (cnt_row && e == 0x00) {
+                    const int key = t0 + t;
+                    const int cat = key < J->n_sink ? 0 : (key < Bc ? 1 : 2);
+                    cnt_row[cat]++;
+                }
+                P[t] = oracle_e4m3_decode(e);
+            } else {
+                P[t] = y;
+            }
+        }
+
+        /* O <- alpha*O + P_fp8 . V_j (FP32 accumulator) */
+        for (int i = 0; i < d; i++)
+            blk[i] = 0.0f;
+        for (int t = 0; t < nt; t++) {
+            const float* vt = V + (int64_t)(t0 + t) * d;
+            for (int i = 0; i < d; i++)
+                blk[i] += P[t] * vt[i];
+        }
+        for (int i = 0; i < d; i++)
+            o[i] = alpha * o[i] + blk[i];
+
+        m = m_new;
+        mc = mc_new;
+    }
+
+    /* epilogue: O / (S * l); lse is the natural-log log-sum-exp of z */
+    const float denom = S * ell;
+    for (int i = 0; i < d; i++)
+        out_row[i] = o[i] / denom;
+    if (lse_row)
+        *lse_row = (float)(((double)mc + log2((double)ell)) * 0.6931471805599453094);
+}
+
+static void* attn_worker(void* arg)
+{
+    attn_job* J = (attn_job*)arg;
+    const int d = J->d, Bc = J->Bc;
+    float* D = (float*)malloc(sizeof(float) * (size_t)Bc);
+    float* P = (float*)malloc(sizeof(float) * (size_t)Bc);
+    float* o = (float*)malloc(sizeof(float) * (size_t)d);
+    float* blk = (float*)malloc(sizeof(float) * (size_t)d);
+    for (;;) {
+        int64_t i;
+        pthread_mutex_lock(&J->lock);
+        i = J->next++;
+        pthread_mutex_unlock(&J->lock);
+        if (i >= J->n_rows)
+            break;
+        const int64_t flat = J->rows ? J->rows[i] : i;
+        attn_row(J, flat, J->out + i * (int64_t)d, J->lse ? J->lse + i : NULL,
+                 J->counts ? J->counts + 3 * i : NULL, D, P, o, blk);
+    }
+    free(D);
+    free(P);
+    free(o);
+    free(blk);
+    return NULL;
+}
+
+static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
+                       int nthreads)
+{
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > 256)
+        nthreads = 256;
+    pthread_t th[256];
+    pthread_mutex_init(lock, NULL);
+    int started = 0;
+    for (int i = 0; i < nthreads; i++) {
+        if (pthread_create(&th[i], NULL, fn, job) != 0)
+            break;
+        started++;
+    }
+    if (started == 0)
+        fn(job);
+    for (int i = 0; i < started; i++)
+        pthread_join(th[i], NULL);
+    pthread_mutex_destroy(lock);
+    return 0;
+}
+
+/*
+ * Algorithm 1 on a list of query rows.
+ *   q: [B][Hq][N][d], k, v: [B][Hkv][N][d], all FP32 host arrays holding the
+ *   exact values the device consumed.
+ *   rows: flat row ids (b*Hq + hq)*N + r (NULL = all B*Hq*N rows in order).
+ *   out: [n_rows][d], lse: [n_rows] (nullable), counts: [n_rows][3]
+ *   (nullable; categories key < n_sink, n_sink <= key < Bc, key >= Bc).
+ *   cast: 0 = no cast (P*S used as is), 1 = E4M3.
+ * Returns 0, or -1 on an invalid argument.
+ */
+int oracle_attn(const float* q, const float* k, const float* v, float* out,
+                float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
+                int d, int causal, int block_kv, int order, float S, int cast,
+                int n_sink, const int64_t* rows, int64_t n_rows, int nthreads)
+{
+    if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
+        d < 1 || Hq % Hkv != 0 || block_kv < 1 || !(S > 0.0f) ||
+        !isfinite(S) || (order != 0 && order != 1) || (cast != 0 && cast != 1) ||
+        n_sink < 0 || n_rows < 0)
+        return -1;
+    if (rows)
+        for (int64_t i = 0; i < n_rows; i++)
+            if (rows[i] < 0 || rows[i] >= (int64_t)B * Hq * N)
+                return -1;
+    if (!rows && n_rows != (int64_t)B * Hq * N)
+        return -1;
+    attn_job J;
+    memset(&J, 0, sizeof(J));
+    J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse; J.counts = counts;
+    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
+    J.Bc = block_kv; J.order = order; J.cast = cast; J.n_sink = n_sink;
+    J.S = S; J.rows = rows; J.n_rows = n_rows; J.nthreads = nthreads;
+    run_threads(attn_worker, &J, &J.lock, nthreads);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Textbook softmax attention in FP64 (no blocks, no cast): the reference the */
+/* MSE is measured against.                                                   */
+/* ------------------------------------------------------------------------- */
+
+typedef struct {
+    const float *q, *k, *v;
+    double* out;
+    double* lse;
+    int B, Hq, Hkv, N, d, causal;
+    const int64_t* rows;
+    int64_t n_rows, next;
+    pthread_mutex_t lock;
+} ref_job;
+
+static void* ref_worker(void* arg)
+{
+    ref_job* J = (ref_job*)arg;
+    const int N = J->N, d = J->d;
+    double* z = (double*)malloc(sizeof(double) * (size_t)N);
+    for (;;) {
+        int64_t i;
+        pthread_mutex_lock(&J->lock);
+        i = J->next++;
+        pthread_mutex_unlock(&J->lock);
+        if (i >= J->n_rows)
+            break;
+        const int64_t flat = J->rows ? J->rows[i] : i;
+        const int64_t bh = flat / N;
+        const int r = (int)(flat % N);
+        const int b = (int)(bh / J->Hq), hq = (int)(bh % J->Hq);
+        const int hk = hq / (J->Hq / J->Hkv);
+        const float* qr = J->q + flat * (int64_t)d;
+        const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
+        const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
+        const int L = J->causal ? r + 1 : N;
+        const double scale = 1.0 / sqrt((double)d);
+        double zmax = -INFINITY;
+        for (int t = 0; t < L; t++) {
+            double acc = 0.0;
+            for (int c = 0; c < d; c++)
+                acc += (double)qr[c] * (double)K[(int64_t)t * d + c];
+            z[t] = acc * scale;
+            if (z[t] > zmax)
+                zmax = z[t];
+        }
+        double ell = 0.0;
+        for (int t = 0; t < L; t++) {
+            z[t] = exp(z[t] - zmax);
+            ell += z[t];
+        }
+        double* o = J->out + i * (int64_t)d;
+        for (int c = 0; c < d; c++)
+            o[c] = 0.0;
+        for (int t = 0; t < L; t++)
+            for (int c = 0; c < d; c++)
+                o[c] += z[t] * (double)V[(int64_t)t * d + c];
+        for (int c = 0; c < d; c++)
+            o[c] /= ell;
+        if (J->lse)
+            J->lse[i] = zmax + log(ell);
+    }
+    free(z);
+    return NULL;
+}
+
+int oracle_ref_fp64(const float* q, const float* k, const float* v,
+                    double* out, double* lse, int B, int Hq, int Hkv, int N,
+                    int d, int causal, const int64_t* rows, int64_t n_rows,
+                    int nthreads)
+{
+    if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
+        d < 1 || Hq % Hkv != 0 || n_rows < 0)
+        return -1;
+    if (rows)
+        for (int64_t i = 0; i < n_rows; i++)
+            if (rows[i] < 0 || rows[i] >= (int64_t)B * Hq * N)
+                return -1;
+    if (!rows && n_rows != (int64_t)B * Hq * N)
+        return -1;
+    ref_job J;
+    memset(&J, 0, sizeof(J));
+    J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse;
+    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
+    J.rows = rows; J.n_rows = n_rows;
+    run_threads(ref_worker, &J, &J.lock, nthreads);
+    return 0;
+}
+
+int oracle_version(void) { return ORACLE_VERSION; }

@@ -1,0 +1,168 @@
+"""Seeded synthetic inputs shaped like the paper's sink workload.
+
+This module only draws and lays out numbers; it contains none of the
+attention arithmetic.  Both the device path and the CPU oracle consume what it
+produces, so they see bit-identical values.
+
+Workload structure (Sec. 3.1): one head per (batch, head) pair, non-sink
+logits s ~ N(0, 1) after the 1/sqrt(d) scaling, the first ``n_sink`` keys lifted
+by Delta (Sec. 3.2: the sink scores carry the same N(0,1) fluctuation as the
+others).  Recipe:
+
+* Q and K entries: N(0, 1) snapped to the 2^-5 grid and clipped to
+  +-(8 - 2^-5).  Every product q_i k_i is then a multiple of 2^-10 below 64 in
+  magnitude, so any dot product over d <= 128 terms is exact in FP32 whatever
+  the summation order, and every entry is exact in bfloat16.
+* The sink offset travels in the last channel: Q[..., d-1] = 1 and
+  K[..., t, d-1] = snap(sqrt(d) * (Delta * [t < n_sink] + b_t)), so the logit of
+  key t gains Delta (+ b_t); b_t ~ N(0, bias_var) when ``bias_var > 0``.  For
+  bfloat16 inputs that channel is additionally rounded to bfloat16 (it is the
+  only channel that can leave the exact range).  The realised sink offset is
+  reported as ``delta_eff``.  Non-sink logits then have variance (d-1)/d.
+* V: float32 N(0, 1) for the FP32 modes; for the fast mode N(0, 1) divided by
+  its per-tensor max |V| and rounded to OCP E4M3 (torch's float8_e4m3fn
+  conversion, round to nearest even), so |V| <= 1.
+
+Seeds: numpy PCG64; ``seed`` is taken as given.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+GRID = 2.0 ** -5
+CLIP = 8.0 - GRID
+
+
+@dataclass
+class AttnInputs:
+    """Host arrays for one problem.
+
+    ``q32``/``k32``/``v32`` are float32 arrays holding exactly the values the
+    device consumes (decoded where the device format is narrower); ``q_dev`` /
+    ``k_dev`` / ``v_dev`` are the arrays in device format (float32, or raw
+    bfloat16 / E4M3 bit patterns as uint16 / uint8).
+    """
+    B: int
+    Hq: int
+    Hkv: int
+    N: int
+    d: int
+    fmt: str                    # "f32" or "bf16_e4m3"
+    delta: float
+    n_sink: int
+    q32: np.ndarray
+    k32: np.ndarray
+    v32: np.ndarray
+    q_dev: np.ndarray
+    k_dev: np.ndarray
+    v_dev: np.ndarray
+    delta_eff: float
+    meta: dict = field(default_factory=dict)
+
+
+def _snap(x: np.ndarray) -> np.ndarray:
+    return np.clip(np.round(x / GRID) * GRID, -CLIP, CLIP).astype(np.float32)
+
+
+def _bf16_round(x: np.ndarray) -> np.ndarray:
+    """Round float32 to the nearest bfloat16 value (ties to even), as float32."""
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.bfloat16).float().numpy()
+
+
+def _bf16_bits(x: np.ndarray) -> np.ndarray:
+    """Raw bfloat16 bit patterns of float32 values that are exact in bfloat16."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    if np.any(u & 0xFFFF):
+        raise AssertionError("value not exact in bfloat16")
+    return (u >> 16).astype(np.uint16)
+
+
+def _e4m3_codes(x: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
+    return t.view(torch.uint8).numpy().copy(), t.float().numpy()
+
+
+def sink_channel(N: int, d: int, delta: float, n_sink: int, bias: np.ndarray | None,
+                 bf16: bool) -> np.ndarray:
+    """Values of K[..., :, d-1] for one KV head (length N)."""
+    off = np.zeros(N, dtype=np.float64)
+    off[:n_sink] = delta
+    if bias is not None:
+        off = off + bias
+    ch = np.round(np.sqrt(d) * off / GRID) * GRID
+    ch = ch.astype(np.float32)
+    if bf16:
+        ch = _bf16_round(ch)
+    return ch
+
+
+def make_inputs(B: int, Hq: int, Hkv: int, N: int, d: int, *, fmt: str, delta: float,
+                seed: int, n_sink: int = 4, bias_var: float = 0.0,
+                sink_channel_on: bool = True) -> AttnInputs:
+    """Draw one problem.  fmt: "f32" (faithful / nocast) or "bf16_e4m3" (fast)."""
+    if fmt not in ("f32", "bf16_e4m3"):
+        raise ValueError(fmt)
+    rng = np.random.Generator(np.random.PCG64(seed))
+    q = _snap(rng.standard_normal((B, Hq, N, d), dtype=np.float32))
+    k = _snap(rng.standard_normal((B, Hkv, N, d), dtype=np.float32))
+    v = rng.standard_normal((B, Hkv, N, d), dtype=np.float32)
+    bias = None
+    if bias_var > 0:
+        bias = rng.standard_normal((B, Hkv, N)) * np.sqrt(bias_var)
+    bf16 = fmt == "bf16_e4m3"
+    delta_eff = float("nan")
+    if sink_channel_on and N > 0:
+        q[..., d - 1] = 1.0
+        for b in range(B):
+            for h in range(Hkv):
+                k[b, h, :, d - 1] = sink_channel(N, d, delta, n_sink,
+                                                 None if bias is None else bias[b, h], bf16)
+        delta_eff = float(sink_channel(max(n_sink, 1), d, delta, n_sink, None, bf16)[0] / np.sqrt(d))
+    meta = {"seed": seed, "bias_var": bias_var}
+    if bf16:
+        amax = float(np.abs(v).max()) if v.size else 1.0
+        v_codes, v32 = _e4m3_codes(v / np.float32(amax))
+        meta["v_amax"] = amax
+        return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v32,
+                          _bf16_bits(q), _bf16_bits(k), v_codes, delta_eff, meta)
+    return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v, q, k, v, delta_eff, meta)
+
+
+def with_delta(inp: AttnInputs, delta: float) -> AttnInputs:
+    """Same base Q/K/V with only the sink keys' channel rewritten for a new Delta
+    (paired runs, as in the paper's paired comparisons).  Requires bias_var == 0."""
+    if inp.meta.get("bias_var", 0.0) > 0:
+        raise ValueError("with_delta needs inputs without a per-key bias")
+    bf16 = inp.fmt == "bf16_e4m3"
+    k32 = inp.k32.copy()
+    ns = min(inp.n_sink, inp.N)
+    ch = sink_channel(max(inp.n_sink, 1), inp.d, delta, inp.n_sink, None, bf16)[:ns]
+    k32[:, :, :ns, inp.d - 1] = ch
+    k_dev = _bf16_bits(k32) if bf16 else k32
+    delta_eff = float(ch[0] / np.sqrt(inp.d)) if ns else float("nan")
+    return AttnInputs(inp.B, inp.Hq, inp.Hkv, inp.N, inp.d, inp.fmt, delta, inp.n_sink,
+                      inp.q32, k32, inp.v32, inp.q_dev, k_dev, inp.v_dev, delta_eff,
+                      dict(inp.meta))
+
+
+def sample_rows(B: int, Hq: int, N: int, tile: int, every: int, seed: int,
+                per_tile: int = 2) -> np.ndarray:
+    """Flat row ids ((b*Hq + h)*N + r) for row-sampled checks: in every head, the
+    first and last query tile in full plus ``per_tile`` random rows from every
+    ``every``-th tile (and always the very last row)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    ntile = (N + tile - 1) // tile
+    rows = []
+    for bh in range(B * Hq):
+        base = bh * N
+        for t in range(ntile):
+            r0, r1 = t * tile, min(N, (t + 1) * tile)
+            if t == 0 or t == ntile - 1:
+                rows.extend(range(base + r0, base + r1))
+            elif t % every == 0:
+                rows.extend(base + rng.integers(r0, r1, size=per_tile))
+        rows.append(base + N - 1)
+    return np.unique(np.asarray(rows, dtype=np.int64))

@@ -1,0 +1,59 @@
+"""Named synthetic workloads (shapes and settings of the measured problems).
+
+Every workload is the paper's sink setting (Sec. 3.1) at a given size; the
+names say what each one is.  ``seed_base`` feeds ``inputs.make_inputs``.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    N: int
+    d: int
+    causal: bool
+    mode: str                 # "faithful" or "fast"
+    block_kv: int
+    deltas: tuple
+    scales: tuple
+    orders: tuple
+    bias_var: float = 0.0
+    seed_base: int = 0
+
+    @property
+    def fmt(self) -> str:
+        return "f32" if self.mode in ("faithful", "nocast") else "bf16_e4m3"
+
+    def flops(self) -> float:
+        """FlashAttention convention: 4*B*Hq*N^2*d, halved under causal masking."""
+        f = 4.0 * self.B * self.Hq * self.N * self.N * self.d
+        return f / 2 if self.causal else f
+
+
+WORKLOADS = {
+    w.name: w for w in [
+        # single head, four sink keys at Delta = 8, both orders, S in {1, 256}
+        Workload("sink_n1024_d64_faithful", 1, 1, 1, 1024, 64, False, "faithful", 64,
+                 (8.0,), (1.0, 256.0), ("forward", "reverse"), seed_base=20260100),
+        # Delta sweep 0..12 over S in {1, 16, 256, 448}, both orders, 8 heads
+        Workload("sink_sweep_h8_n4096_d128_faithful", 1, 8, 8, 4096, 128, False, "faithful", 128,
+                 tuple(float(x) for x in range(13)), (1.0, 16.0, 256.0, 448.0),
+                 ("forward", "reverse"), seed_base=20260200),
+        # causal MHA prefill, bf16 Q/K, e4m3 V, Delta = 7, reverse, S = 256
+        Workload("causal_mha_b4_h32_n8192_d128_fast", 4, 32, 32, 8192, 128, True, "fast", 128,
+                 (7.0,), (256.0,), ("reverse",), seed_base=20260300),
+        # causal GQA 64/8 heads at 32k, Delta = 9, S in {1, 256}, both orders
+        Workload("causal_gqa_h64kv8_n32768_d128_fast", 1, 64, 8, 32768, 128, True, "fast", 128,
+                 (9.0,), (1.0, 256.0), ("forward", "reverse"), seed_base=20260400),
+        # causal GQA 32/8 heads at 128k, Delta = 10 plus a N(0, 0.5) per-key bias
+        Workload("causal_gqa_h32kv8_n131072_d128_fast_bias", 1, 32, 8, 131072, 128, True, "fast",
+                 128, (10.0,), (256.0,), ("reverse",), bias_var=0.5, seed_base=20260500),
+    ]
+}
+
+HEADLINE = "causal_mha_b4_h32_n8192_d128_fast"
