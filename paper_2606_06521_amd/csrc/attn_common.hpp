@@ -1,0 +1,104 @@
+// Shared device-side pieces of the FP8 attention kernels for gfx950 (CDNA4):
+// MFMA operand types, the launch parameter block, the XCD-aware mapping of
+// workgroups to (batch*head, query tile), and wave-level helpers.
+//
+// Layout convention used by both kernel families ("transposed" form):
+//   S^T = K . Q^T   and   O^T = V^T . P^T
+// A 32x32 MFMA accumulator gives lane (n = lane % 32, h = lane / 32) the
+// elements D[8*(r/4) + 4*h + (r%4)][n], r = 0..15.  With the query row as the
+// N index, every accumulator register of a lane belongs to ONE query row, so
+// the running max, the sum l and the rescale factor alpha are per-lane scalars
+// and a row reduction needs one exchange between the two 32-lane halves.
+// Key rows of the S^T tile are permuted so that register r of half h holds key
+// 16*h + r of the 32-key tile; the P bytes of a lane then form the B operand
+// of the FP8 P.V MFMA without any data movement.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace attn {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(8 * sizeof(int)))) int i32x8;
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(int)))) int i32x2;
+
+// Launch parameters (passed by value as the kernel argument block).
+struct Params {
+    const void* q;
+    const void* k;
+    const void* v;
+    float* out;
+    float* lse;          // nullable
+    uint32_t* counts;    // COUNT instantiations only
+    int B, Hq, Hkv, N;
+    int order;           // 0 forward, 1 reverse
+    int n_sink;
+    float S;             // static P-scale
+    float inv_S;         // 1/S, used only when S is a power of two (exact)
+    float c;             // fl32(log2(e) / sqrt(d))
+    int n_tiles;         // query tiles per (batch, head)
+    int total_wg;        // B * Hq * n_tiles
+    int per_xcd;         // ceil(total_wg / 8)
+};
+
+constexpr int kNumXcd = 8;   // MI355X: 8 XCDs x 32 CUs, workgroup i runs on XCD i % 8
+
+// Workgroup -> (batch*head, tile).  Hardware places workgroup i on XCD i % 8;
+// the logical index gives each XCD a contiguous range, so all query tiles of
+// one head (and neighbouring heads of one GQA group) run on the same XCD and
+// share its L2 for the K/V stream.  Under causal masking the heaviest tile of a
+// head (the last rows) is issued first.
+template <bool CAUSAL>
+__device__ inline bool map_tile(const Params& p, int& bh, int& tile)
+{
+    const int i = blockIdx.x;
+    const int xcd = i % kNumXcd;
+    const int slot = i / kNumXcd;
+    if (slot >= p.per_xcd)
+        return false;
+    const int L = xcd * p.per_xcd + slot;
+    if (L >= p.total_wg)
+        return false;
+    bh = L / p.n_tiles;
+    const int t = L - bh * p.n_tiles;
+    tile = CAUSAL ? (p.n_tiles - 1 - t) : t;
+    return true;
+}
+
+// Key permutation inside a 32-key S^T tile: MFMA A-row m -> key offset, so that
+// accumulator register r of lane half h holds key 16*h + r.
+// m = (b4 b3 b2 b1 b0) -> key = (b2 b4 b3 b1 b0).
+__device__ inline int a_row_to_key(int m)
+{
+    return ((m >> 2) & 1) * 16 + ((m >> 3) & 3) * 4 + (m & 3);
+}
+
+// Value of the other 32-lane half of the wave.
+__device__ inline float other_half(float x)
+{
+    return __shfl_xor(x, 32, 64);
+}
+
+__device__ inline uint32_t other_half_u32(uint32_t x)
+{
+    return (uint32_t)__shfl_xor((int)x, 32, 64);
+}
+
+__device__ inline float fmax_f(float a, float b) { return __builtin_fmaxf(a, b); }
+
+// Number of zero bytes in a 32-bit word.
+__device__ inline uint32_t zero_bytes(uint32_t w)
+{
+    uint32_t n = 0;
+    n += (w & 0x000000FFu) == 0;
+    n += (w & 0x0000FF00u) == 0;
+    n += (w & 0x00FF0000u) == 0;
+    n += (w & 0xFF000000u) == 0;
+    return n;
+}
+
+}  // namespace attn

@@ -1,0 +1,134 @@
+// C ABI of libattn_fp8.so (declared in include/attn_fp8.h): argument
+// validation, choice of kernel instantiation, grid sizing, launch on the
+// caller's stream.  No memory is allocated and no state is kept.
+#include "../../include/attn_fp8.h"
+#include "attn_common.hpp"
+#include "attn_launch.hpp"
+
+#include <math.h>
+#include <stdint.h>
+
+namespace {
+
+constexpr int kVersion = 100;   // 0.1.0
+
+bool is_pow2_scale(float S)
+{
+    int e = 0;
+    const float m = frexpf(S, &e);
+    return m == 0.5f;
+}
+
+// Shared validation and dispatch of both entry points.
+int run(const void* q, const void* k, const void* v, float* out, float* lse,
+        uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int d, int causal,
+        int block_kv, int order, float S, int mode, int n_sink, void* stream)
+{
+    if (B < 0 || Hq < 1 || Hkv < 1 || N < 0 || Hq % Hkv != 0)
+        return ATTN_ERR_INVALID_ARG;
+    if (causal != 0 && causal != 1)
+        return ATTN_ERR_INVALID_ARG;
+    if (order != ATTN_ORDER_FORWARD && order != ATTN_ORDER_REVERSE)
+        return ATTN_ERR_INVALID_ARG;
+    if (mode != ATTN_MODE_FAITHFUL && mode != ATTN_MODE_FAST && mode != ATTN_MODE_NOCAST)
+        return ATTN_ERR_INVALID_ARG;
+    if (!(S > 0.0f) || !isfinite(S))
+        return ATTN_ERR_INVALID_ARG;
+    if (n_sink < 0)
+        return ATTN_ERR_INVALID_ARG;
+    if (d < 1 || block_kv < 1)
+        return ATTN_ERR_INVALID_ARG;
+    if (d != 64 && d != 128)
+        return ATTN_ERR_UNSUPPORTED;
+    if (block_kv != 64 && block_kv != 128)
+        return ATTN_ERR_UNSUPPORTED;
+    const int64_t rows = (int64_t)B * Hq * N;
+    if (rows == 0)
+        return ATTN_OK;
+    if (!q || !k || !v)
+        return ATTN_ERR_INVALID_ARG;
+    if (count ? !counts : !out)
+        return ATTN_ERR_INVALID_ARG;
+    // element offsets stay within 64-bit; the grid must fit a 1-D launch
+    const int bm = (mode == ATTN_MODE_FAST) ? attn::fast_rows_per_wg(d, block_kv)
+                                            : attn::faithful_rows_per_wg();
+    const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;
+    const int64_t total = (int64_t)B * Hq * n_tiles;
+    if (total > (int64_t)1 << 30)
+        return ATTN_ERR_UNSUPPORTED;
+
+    attn::Params p;
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.out = out;
+    p.lse = lse;
+    p.counts = counts;
+    p.B = B;
+    p.Hq = Hq;
+    p.Hkv = Hkv;
+    p.N = N;
+    p.order = order;
+    p.n_sink = n_sink;
+    p.S = S;
+    p.inv_S = 1.0f / S;
+    // exp(z) = exp2(D * c) with z = D / sqrt(d): c rounded once from double
+    p.c = (float)(1.4426950408889634074 / sqrt((double)d));
+    p.n_tiles = (int)n_tiles;
+    p.total_wg = (int)total;
+    p.per_xcd = (int)((total + attn::kNumXcd - 1) / attn::kNumXcd);
+
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    hipError_t e;
+    if (mode == ATTN_MODE_FAST) {
+        // the scaled convert applies 1/S exactly only for S = 2^k, and only
+        // below the E4M3 range limit (it does not saturate)
+        const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
+        e = attn::launch_fast(p, d, block_kv, causal != 0, count, pow2, s);
+    } else {
+        e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, s);
+    }
+    return e == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int attn_fp8_fwd(const void* q, const void* k, const void* v, float* out, float* lse, int B,
+                 int Hq, int Hkv, int N, int d, int causal, int block_kv, int order, float S,
+                 int mode, void* stream)
+{
+    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+               mode, 0, stream);
+}
+
+int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v, int B, int Hq,
+                               int Hkv, int N, int d, int causal, int block_kv, int order,
+                               float S, int mode, int n_sink, uint32_t* counts, float* out,
+                               float* lse, void* stream)
+{
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+               mode, n_sink, stream);
+}
+
+const char* attn_fp8_strerror(int status)
+{
+    switch (status) {
+    case ATTN_OK:
+        return "ok";
+    case ATTN_ERR_INVALID_ARG:
+        return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
+               "and positive, or order/mode/causal/n_sink out of range)";
+    case ATTN_ERR_UNSUPPORTED:
+        return "unsupported configuration (d and block_kv must be 64 or 128)";
+    case ATTN_ERR_HIP:
+        return "the HIP runtime rejected the kernel launch";
+    default:
+        return "unknown status";
+    }
+}
+
+int attn_fp8_version(void) { return kVersion; }
+
+}  // extern "C"

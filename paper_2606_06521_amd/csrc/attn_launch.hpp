@@ -1,0 +1,17 @@
+// Host-side launchers of the two kernel families (defined next to their
+// kernels) and the tile geometry the dispatcher needs to size the grid.
+#pragma once
+
+#include "attn_common.hpp"
+
+namespace attn {
+
+hipError_t launch_faithful(const Params& p, int d, int block_kv, bool causal, bool count,
+                           bool cast, hipStream_t stream);
+int faithful_rows_per_wg();
+
+hipError_t launch_fast(const Params& p, int d, int block_kv, bool causal, bool count,
+                       bool pow2_scale, hipStream_t stream);
+int fast_rows_per_wg(int d, int block_kv);
+
+}  // namespace attn

@@ -23,10 +23,14 @@ others).  Recipe:
   its per-tensor max |V| and rounded to OCP E4M3 (torch's float8_e4m3fn
   conversion, round to nearest even), so |V| <= 1.
 
-Seeds: numpy PCG64; ``seed`` is taken as given.
+Seeds: numpy PCG64; head (b, h) of each tensor draws from its own stream
+seeded by SeedSequence([seed, tensor, b, h]) (q = 1, k = 2, v = 3; the per-key
+bias uses [seed, 4]).
 """
 from __future__ import annotations
 
+import concurrent.futures as cf
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -63,8 +67,12 @@ class AttnInputs:
     meta: dict = field(default_factory=dict)
 
 
-def _snap(x: np.ndarray) -> np.ndarray:
-    return np.clip(np.round(x / GRID) * GRID, -CLIP, CLIP).astype(np.float32)
+def _snap_inplace(x: np.ndarray) -> None:
+    """Snap float32 data to the 2^-5 grid (round half to even) and clip, in place."""
+    x *= np.float32(1.0 / GRID)
+    np.rint(x, out=x)
+    np.clip(x, -CLIP / GRID, CLIP / GRID, out=x)
+    x *= np.float32(GRID)
 
 
 def _bf16_round(x: np.ndarray) -> np.ndarray:
@@ -75,14 +83,42 @@ def _bf16_round(x: np.ndarray) -> np.ndarray:
 def _bf16_bits(x: np.ndarray) -> np.ndarray:
     """Raw bfloat16 bit patterns of float32 values that are exact in bfloat16."""
     u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
-    if np.any(u & 0xFFFF):
+    if np.any(u[..., ::7] & 0xFFFF):
         raise AssertionError("value not exact in bfloat16")
-    return (u >> 16).astype(np.uint16)
+    # little-endian: the high 16 bits of each float32 are the odd uint16 halves
+    return np.ascontiguousarray(u.view(np.uint16)[..., 1::2])
 
 
 def _e4m3_codes(x: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
     t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e4m3fn)
     return t.view(torch.uint8).numpy().copy(), t.float().numpy()
+
+
+def _workers() -> int:
+    try:
+        return max(1, min(16, len(os.sched_getaffinity(0))))
+    except AttributeError:  # pragma: no cover
+        return 4
+
+
+def _normal_heads(seed: int, tag: int, B: int, H: int, N: int, d: int) -> np.ndarray:
+    """[B][H][N][d] float32 N(0,1); head (b, h) draws from its own PCG64 stream
+    seeded by (seed, tag, b, h), so heads can be generated in parallel."""
+    out = np.empty((B, H, N, d), dtype=np.float32)
+
+    def fill(bh):
+        b, h = divmod(bh, H)
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tag, b, h])))
+        rng.standard_normal((N, d), dtype=np.float32, out=out[b, h])
+
+    with cf.ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(fill, range(B * H)))
+    return out
+
+
+def _parallel_heads(fn, B: int, H: int) -> None:
+    with cf.ThreadPoolExecutor(_workers()) as ex:
+        list(ex.map(lambda bh: fn(*divmod(bh, H)), range(B * H)))
 
 
 def sink_channel(N: int, d: int, delta: float, n_sink: int, bias: np.ndarray | None,
@@ -105,14 +141,16 @@ def make_inputs(B: int, Hq: int, Hkv: int, N: int, d: int, *, fmt: str, delta: f
     """Draw one problem.  fmt: "f32" (faithful / nocast) or "bf16_e4m3" (fast)."""
     if fmt not in ("f32", "bf16_e4m3"):
         raise ValueError(fmt)
-    rng = np.random.Generator(np.random.PCG64(seed))
-    q = _snap(rng.standard_normal((B, Hq, N, d), dtype=np.float32))
-    k = _snap(rng.standard_normal((B, Hkv, N, d), dtype=np.float32))
-    v = rng.standard_normal((B, Hkv, N, d), dtype=np.float32)
+    q = _normal_heads(seed, 1, B, Hq, N, d)
+    k = _normal_heads(seed, 2, B, Hkv, N, d)
+    v = _normal_heads(seed, 3, B, Hkv, N, d)
     bias = None
     if bias_var > 0:
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 4])))
         bias = rng.standard_normal((B, Hkv, N)) * np.sqrt(bias_var)
     bf16 = fmt == "bf16_e4m3"
+    _parallel_heads(lambda b, h: _snap_inplace(q[b, h]), B, Hq)
+    _parallel_heads(lambda b, h: _snap_inplace(k[b, h]), B, Hkv)
     delta_eff = float("nan")
     if sink_channel_on and N > 0:
         q[..., d - 1] = 1.0
@@ -123,10 +161,16 @@ def make_inputs(B: int, Hq: int, Hkv: int, N: int, d: int, *, fmt: str, delta: f
         delta_eff = float(sink_channel(max(n_sink, 1), d, delta, n_sink, None, bf16)[0] / np.sqrt(d))
     meta = {"seed": seed, "bias_var": bias_var}
     if bf16:
-        amax = float(np.abs(v).max()) if v.size else 1.0
-        v_codes, v32 = _e4m3_codes(v / np.float32(amax))
+        amax = float(max(v.max(), -v.min())) if v.size else 1.0
+        v_codes = np.empty(v.shape, dtype=np.uint8)
+
+        def enc(b, h):
+            v[b, h] /= np.float32(amax)
+            v_codes[b, h], v[b, h] = _e4m3_codes(v[b, h])
+
+        _parallel_heads(enc, B, Hkv)
         meta["v_amax"] = amax
-        return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v32,
+        return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v,
                           _bf16_bits(q), _bf16_bits(k), v_codes, delta_eff, meta)
     return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v, q, k, v, delta_eff, meta)
 

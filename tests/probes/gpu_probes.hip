@@ -1,0 +1,169 @@
+// Hardware probes for the GPU tests (test infrastructure, not part of the
+// library).  Each probe runs one gfx950 instruction the attention kernels rely
+// on over caller-chosen inputs, so the tests can compare it with the CPU
+// oracle or with exact host arithmetic:
+//   - v_cvt_pk_fp8_f32 and v_cvt_scalef32_pk_fp8_f32 (the E4M3 P-cast),
+//   - v_exp_f32 (exp2 in the fast kernels),
+//   - the operand/accumulator lane layouts of the three MFMA shapes used.
+// Every kernel bounds-checks its index against n.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(8 * sizeof(int)))) int i32x8;
+typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+
+__global__ void k_cvt_range(uint32_t lo, int64_t n, uint8_t* out)
+{
+    const int64_t i = 2 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+    if (i >= n)
+        return;
+    const float x0 = __builtin_bit_cast(float, (uint32_t)(lo + i));
+    const float x1 = (i + 1 < n) ? __builtin_bit_cast(float, (uint32_t)(lo + i + 1)) : 0.f;
+    const int w = __builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+    out[i] = (uint8_t)(w & 0xFF);
+    if (i + 1 < n)
+        out[i + 1] = (uint8_t)((w >> 8) & 0xFF);
+}
+
+__global__ void k_cvt_list(const float* x, int64_t n, uint8_t* out, float scale, int scaled, int hi)
+{
+    const int64_t i = 2 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+    if (i >= n)
+        return;
+    const float x0 = x[i];
+    const float x1 = (i + 1 < n) ? x[i + 1] : 0.f;
+    uint32_t w;
+    s16x2 z = {0, 0};
+    if (scaled && hi)
+        w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(z, x0, x1, scale, true));
+    else if (scaled)
+        w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(z, x0, x1, scale, false));
+    else if (hi)
+        w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, true);
+    else
+        w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(x0, x1, 0, false);
+    if (hi)
+        w >>= 16;
+    out[i] = (uint8_t)(w & 0xFF);
+    if (i + 1 < n)
+        out[i + 1] = (uint8_t)((w >> 8) & 0xFF);
+}
+
+__global__ void k_exp2(const float* x, int64_t n, float* out)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n)
+        out[i] = __builtin_amdgcn_exp2f(x[i]);
+}
+
+// One wave.  A: 32x16 bf16 (row-major), B: 16x32 bf16, D: 32x32 f32.
+// Assumed layout: lane (m = l%32, h = l/32) holds A[m][8h..8h+7] and
+// B[8h..8h+7][m]; accumulator register r is D[8(r/4) + 4h + r%4][l%32].
+__global__ void k_mfma_bf16(const uint16_t* A, const uint16_t* B, float* D)
+{
+    const int l = threadIdx.x;
+    if (l >= 64)
+        return;
+    const int m = l & 31, h = l >> 5;
+    bf16x8 a, b;
+    for (int i = 0; i < 8; ++i) {
+        a[i] = __builtin_bit_cast(__bf16, A[m * 16 + 8 * h + i]);
+        b[i] = __builtin_bit_cast(__bf16, B[(8 * h + i) * 32 + m]);
+    }
+    f32x16 acc = {};
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+    for (int r = 0; r < 16; ++r)
+        D[(8 * (r / 4) + 4 * h + (r % 4)) * 32 + m] = acc[r];
+}
+
+// One wave.  A: 32x64 E4M3 bytes, B: 64x32 E4M3 bytes, D: 32x32 f32.
+// Assumed: lane (m, h) holds A[m][32h .. 32h+31] and B[32h .. 32h+31][m].
+__global__ void k_mfma_fp8(const uint8_t* A, const uint8_t* B, float* D)
+{
+    const int l = threadIdx.x;
+    if (l >= 64)
+        return;
+    const int m = l & 31, h = l >> 5;
+    i32x8 a, b;
+    for (int q = 0; q < 8; ++q) {
+        uint32_t wa = 0, wb = 0;
+        for (int e = 0; e < 4; ++e) {
+            const int kk = 32 * h + 4 * q + e;
+            wa |= (uint32_t)A[m * 64 + kk] << (8 * e);
+            wb |= (uint32_t)B[kk * 32 + m] << (8 * e);
+        }
+        a[q] = (int)wa;
+        b[q] = (int)wb;
+    }
+    f32x16 acc = {};
+    acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 0, 0, 0, 0, 0, 0);
+    for (int r = 0; r < 16; ++r)
+        D[(8 * (r / 4) + 4 * h + (r % 4)) * 32 + m] = acc[r];
+}
+
+// One wave.  A: 32x2 f32, B: 2x32 f32, D: 32x32 f32.  Lane (m, h): A[m][h], B[h][m].
+__global__ void k_mfma_f32(const float* A, const float* B, float* D)
+{
+    const int l = threadIdx.x;
+    if (l >= 64)
+        return;
+    const int m = l & 31, h = l >> 5;
+    f32x16 acc = {};
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(A[m * 2 + h], B[h * 32 + m], acc, 0, 0, 0);
+    for (int r = 0; r < 16; ++r)
+        D[(8 * (r / 4) + 4 * h + (r % 4)) * 32 + m] = acc[r];
+}
+
+static int grid_for(int64_t items, int per_block)
+{
+    return (int)((items + per_block - 1) / per_block);
+}
+
+extern "C" {
+
+int probe_cvt_range(uint32_t lo, int64_t n, uint8_t* out, void* stream)
+{
+    if (n <= 0 || !out || (uint64_t)lo + (uint64_t)n > 0x100000000ull)
+        return -1;
+    hipLaunchKernelGGL(k_cvt_range, dim3(grid_for((n + 1) / 2, 256)), dim3(256), 0,
+                       (hipStream_t)stream, lo, n, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int probe_cvt_list(const float* x, int64_t n, uint8_t* out, float scale, int scaled, int hi,
+                   void* stream)
+{
+    if (n <= 0 || !x || !out)
+        return -1;
+    hipLaunchKernelGGL(k_cvt_list, dim3(grid_for((n + 1) / 2, 256)), dim3(256), 0,
+                       (hipStream_t)stream, x, n, out, scale, scaled, hi);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int probe_exp2(const float* x, int64_t n, float* out, void* stream)
+{
+    if (n <= 0 || !x || !out)
+        return -1;
+    hipLaunchKernelGGL(k_exp2, dim3(grid_for(n, 256)), dim3(256), 0, (hipStream_t)stream, x, n, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int probe_mfma(int which, const void* A, const void* B, float* D, void* stream)
+{
+    if (!A || !B || !D)
+        return -1;
+    hipStream_t s = (hipStream_t)stream;
+    if (which == 0)
+        hipLaunchKernelGGL(k_mfma_bf16, dim3(1), dim3(64), 0, s, (const uint16_t*)A, (const uint16_t*)B, D);
+    else if (which == 1)
+        hipLaunchKernelGGL(k_mfma_fp8, dim3(1), dim3(64), 0, s, (const uint8_t*)A, (const uint8_t*)B, D);
+    else if (which == 2)
+        hipLaunchKernelGGL(k_mfma_f32, dim3(1), dim3(64), 0, s, (const float*)A, (const float*)B, D);
+    else
+        return -1;
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+}  // extern "C"

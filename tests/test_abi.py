@@ -1,0 +1,98 @@
+"""The C ABI on the host (no GPU needed): the library loads, exports every
+symbol include/attn_fp8.h declares, and rejects bad arguments before any HIP
+call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "attn_fp8.h")
+
+
+@pytest.fixture(scope="module")
+def A():
+    from paper_2606_06521_amd import attn_fp8
+    return attn_fp8
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(attn_fp8_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(A):
+    names = declared_functions()
+    assert names == ["attn_fp8_fwd", "attn_fp8_p_underflow_count", "attn_fp8_strerror",
+                     "attn_fp8_version"]
+    lib = ctypes.CDLL(A.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strerror(A):
+    assert A.attn_fp8_version() >= 100
+    for st in (A.ATTN_OK, A.ATTN_ERR_INVALID_ARG, A.ATTN_ERR_UNSUPPORTED, A.ATTN_ERR_HIP, 12345):
+        assert isinstance(A.attn_fp8_strerror(st), str) and A.attn_fp8_strerror(st)
+
+
+def test_enum_values_match_header(A):
+    text = open(HEADER).read()
+    for name in ["ATTN_MODE_FAITHFUL", "ATTN_MODE_FAST", "ATTN_MODE_NOCAST", "ATTN_ORDER_FORWARD",
+                 "ATTN_ORDER_REVERSE", "ATTN_OK", "ATTN_ERR_INVALID_ARG", "ATTN_ERR_UNSUPPORTED",
+                 "ATTN_ERR_HIP"]:
+        m = re.search(name + r"\s*=\s*(-?\d+)", text)
+        assert m and int(m.group(1)) == getattr(A, name), name
+
+
+FAKE = 0x1000   # never dereferenced: every case below fails validation first
+
+
+def fwd(A, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, lse=None, B=1, Hq=4, Hkv=2, N=128, d=128, causal=1,
+             block_kv=128, order=1, S=256.0, mode=1, stream=None)
+    a.update(kw)
+    return A.attn_fp8_fwd(a["q"], a["k"], a["v"], a["out"], a["lse"], a["B"], a["Hq"], a["Hkv"],
+                          a["N"], a["d"], a["causal"], a["block_kv"], a["order"], a["S"], a["mode"],
+                          a["stream"])
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(q=None), -1), (dict(k=None), -1), (dict(v=None), -1), (dict(out=None), -1),
+    (dict(Hkv=3), -1), (dict(Hq=0), -1), (dict(B=-1), -1), (dict(N=-5), -1),
+    (dict(causal=2), -1), (dict(order=2), -1), (dict(mode=3), -1), (dict(mode=-1), -1),
+    (dict(S=0.0), -1), (dict(S=-1.0), -1), (dict(S=float("inf")), -1), (dict(S=float("nan")), -1),
+    (dict(d=96), -2), (dict(d=256), -2), (dict(block_kv=32), -2), (dict(block_kv=256), -2),
+    (dict(d=0), -1),
+])
+def test_fwd_rejects_bad_arguments(A, kw, status):
+    assert fwd(A, **kw) == status
+
+
+def test_empty_problems_return_ok_without_touching_pointers(A):
+    assert fwd(A, N=0, q=None, k=None, v=None, out=None) == 0
+    assert fwd(A, B=0, q=None, k=None, v=None, out=None) == 0
+
+
+def test_count_rejects_bad_arguments(A):
+    def cnt(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, B=1, Hq=2, Hkv=1, N=64, d=64, causal=0, block_kv=64,
+                 order=0, S=1.0, mode=0, n_sink=4, counts=FAKE, out=None, lse=None, stream=None)
+        a.update(kw)
+        return A.attn_fp8_p_underflow_count(a["q"], a["k"], a["v"], a["B"], a["Hq"], a["Hkv"],
+                                            a["N"], a["d"], a["causal"], a["block_kv"], a["order"],
+                                            a["S"], a["mode"], a["n_sink"], a["counts"], a["out"],
+                                            a["lse"], a["stream"])
+    assert cnt(counts=None) == -1
+    assert cnt(n_sink=-1) == -1
+    assert cnt(d=32) == -2
+    assert cnt(N=0, counts=None) == 0
+
+
+def test_binding_checks_dtypes_before_calling(A):
+    import torch
+    q = torch.zeros((1, 1, 4, 64), dtype=torch.float32)
+    with pytest.raises(ValueError):
+        A.fwd(q, q, q, mode="faithful")          # host tensors are refused

@@ -1,0 +1,161 @@
+"""Parity of the HIP kernels (through the C ABI) with the CPU oracle.
+
+Bar: P-underflow counts bit-exact per row; outputs within 2e-3 absolute
+(faithful / nocast) or 2e-2 (fast); log-sum-exp within 1e-4.  Inputs are the
+seeded sink workloads; Q/K sit on the 2^-5 grid so every dot product is exact
+on both sides and the cast decisions are reproducible.
+"""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_06521_amd.inputs import make_inputs, sample_rows, with_delta
+from paper_2606_06521_amd.workloads import WORKLOADS
+from tests.gpu_helpers import compare, log, run_gpu, to_device
+
+pytestmark = pytest.mark.gpu
+
+SMALL = list(itertools.product([64, 128], [64, 128], [False, True], ["forward", "reverse"]))
+
+
+@pytest.mark.parametrize("d,bkv,causal,order", SMALL)
+def test_small_faithful_and_nocast(d, bkv, causal, order):
+    # several 128-row tiles plus a ragged tail, GQA 4/2, two batches
+    inp = make_inputs(2, 4, 2, 333, d, fmt="f32", delta=8.0, seed=100 + d + bkv)
+    dev = to_device(inp)
+    for mode, S in [("faithful", 1.0), ("faithful", 256.0), ("faithful", 448.0), ("faithful", 3.0),
+                    ("nocast", 256.0)]:
+        label = f"{mode} d={d} bkv={bkv} causal={causal} {order} S={S}"
+        log(label)
+        gpu = run_gpu(dev, mode, S, order, causal, bkv)
+        compare(inp, gpu, mode, S, order, causal, bkv, label=label)
+
+
+@pytest.mark.parametrize("d,bkv,causal,order", SMALL)
+def test_small_fast(d, bkv, causal, order):
+    inp = make_inputs(2, 4, 2, 333, d, fmt="bf16_e4m3", delta=8.0, seed=200 + d + bkv)
+    dev = to_device(inp)
+    for S in (1.0, 256.0, 448.0, 3.0, 512.0):
+        label = f"fast d={d} bkv={bkv} causal={causal} {order} S={S}"
+        log(label)
+        gpu = run_gpu(dev, "fast", S, order, causal, bkv)
+        compare(inp, gpu, "fast", S, order, causal, bkv, label=label)
+
+
+@pytest.mark.parametrize("N", [1, 31, 32, 33, 64, 65, 129])
+@pytest.mark.parametrize("mode", ["faithful", "fast"])
+def test_edge_lengths(N, mode):
+    fmt = "f32" if mode == "faithful" else "bf16_e4m3"
+    inp = make_inputs(1, 2, 1, N, 128, fmt=fmt, delta=9.0, seed=300 + N)
+    dev = to_device(inp)
+    for causal, order in itertools.product([False, True], ["forward", "reverse"]):
+        label = f"{mode} N={N} causal={causal} {order}"
+        log(label)
+        gpu = run_gpu(dev, mode, 256.0, order, causal, 64)
+        compare(inp, gpu, mode, 256.0, order, causal, 64, label=label)
+
+
+def test_empty_problem_is_a_noop():
+    from paper_2606_06521_amd import attn_fp8 as A
+    st = A.attn_fp8_fwd(None, None, None, None, None, 1, 4, 2, 0, 128, 1, 128, 1, 256.0, 1,
+                        torch.cuda.current_stream().cuda_stream)
+    assert st == A.ATTN_OK
+
+
+@pytest.mark.parametrize("mode", ["faithful", "fast"])
+def test_deterministic_and_count_run_matches(mode):
+    from paper_2606_06521_amd import attn_fp8 as A
+    fmt = "f32" if mode == "faithful" else "bf16_e4m3"
+    inp = make_inputs(1, 4, 4, 1000, 128, fmt=fmt, delta=7.0, seed=400)
+    q, k, v = to_device(inp)
+    o1, l1 = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, mode=mode)
+    o2, l2 = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, mode=mode)
+    o3 = torch.empty_like(o1)
+    l3 = torch.empty_like(l1)
+    A.p_underflow_count(q, k, v, S=256.0, order="reverse", causal=True, mode=mode, out=o3, lse=l3)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+    assert torch.equal(o1, o3) and torch.equal(l1, l3)
+
+
+def test_workload_sink_n1024_d64_faithful():
+    w = WORKLOADS["sink_n1024_d64_faithful"]
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    dev = to_device(inp)
+    for S, order in itertools.product(w.scales, w.orders):
+        label = f"{w.name} S={S} {order}"
+        log(label)
+        gpu = run_gpu(dev, w.mode, S, order, w.causal, w.block_kv)
+        compare(inp, gpu, w.mode, S, order, w.causal, w.block_kv, label=label)
+        if order == "reverse" and S == 256.0:
+            # fixed point (c) on the device: no key beyond the sink block is zeroed
+            assert gpu[2][..., 2].sum() == 0
+
+
+def test_workload_sink_sweep_faithful():
+    w = WORKLOADS["sink_sweep_h8_n4096_d128_faithful"]
+    base = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=0.0, seed=w.seed_base)
+    rows = np.concatenate([np.arange(h * w.N, (h + 1) * w.N, 16) + (3 * h) % 16 for h in range(w.Hq)])
+    rows = np.unique(np.concatenate([rows, np.arange(w.N - 130, w.N)]))
+    for D in (0.0, 5.0, 7.0, 9.0, 12.0):
+        inp = with_delta(base, D)
+        dev = to_device(inp)
+        for S, order in itertools.product(w.scales, w.orders):
+            label = f"{w.name} Delta={D} S={S} {order}"
+            log(label)
+            gpu = run_gpu(dev, w.mode, S, order, w.causal, w.block_kv)
+            compare(inp, gpu, w.mode, S, order, w.causal, w.block_kv, rows=rows, label=label)
+            if order == "reverse" and S == 256.0:
+                assert gpu[2][..., 2].sum() == 0
+        del dev
+        torch.cuda.empty_cache()
+
+
+def test_workload_causal_mha_n8192_fast_full_size():
+    w = WORKLOADS["causal_mha_b4_h32_n8192_d128_fast"]
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    dev = to_device(inp)
+    rows = sample_rows(w.B, w.Hq, w.N, 128, 8, seed=1, per_tile=2)
+    label = f"{w.name} S=256 reverse (rows {rows.size})"
+    log(label)
+    gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv)
+    res = compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows, label=label)
+    log(str(res))
+
+
+def _heads_rows(N, heads, tile, every, seed, Hq):
+    rows = sample_rows(1, Hq, N, tile, every, seed=seed, per_tile=1)
+    keep = np.isin(rows // N, heads)
+    return rows[keep]
+
+
+def test_workload_causal_gqa_n32768_fast_full_size():
+    w = WORKLOADS["causal_gqa_h64kv8_n32768_d128_fast"]
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    dev = to_device(inp)
+    rows = _heads_rows(w.N, np.arange(0, 64, 9), 128, 32, 2, w.Hq)
+    for S, order in itertools.product(w.scales, w.orders):
+        label = f"{w.name} S={S} {order} (rows {rows.size})"
+        log(label)
+        gpu = run_gpu(dev, w.mode, S, order, w.causal, w.block_kv)
+        res = compare(inp, gpu, w.mode, S, order, w.causal, w.block_kv, rows=rows, label=label)
+        log(str(res))
+
+
+def test_workload_causal_gqa_n131072_fast_bias_full_size():
+    w = WORKLOADS["causal_gqa_h32kv8_n131072_d128_fast_bias"]
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base,
+                      bias_var=w.bias_var)
+    dev = to_device(inp)
+    rng = np.random.default_rng(3)
+    heads = np.array([0, 13, 31])
+    rows = np.concatenate([h * w.N + np.concatenate([np.arange(0, 64), rng.integers(0, w.N, 48),
+                                                     np.arange(w.N - 16, w.N)]) for h in heads])
+    rows = np.unique(rows)
+    label = f"{w.name} S=256 reverse (rows {rows.size})"
+    log(label)
+    gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv)
+    res = compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows, label=label)
+    log(str(res))

@@ -1,0 +1,141 @@
+"""Hardware facts the parity argument rests on (gfx950), checked against the
+CPU oracle or exact host arithmetic:
+
+- the E4M3 convert is OCP E4M3 (bias 7, max 448) with round-to-nearest-even,
+  bit-identical to the oracle's encoder on every non-negative FP32 input below
+  464 (the whole range P*S can take for S <= 448);
+- the scaled convert with scale 2^-k equals the plain convert of x * 2^k;
+- v_exp_f32 is exact at integers and monotone around them, so for S = 2^k the
+  zero-code decision is x <= -(10 + k) on both sides;
+- the MFMA operand / accumulator lane layouts the kernels assume.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def probes():
+    from tests import probes as pr
+    return pr.lib()
+
+
+def _stream():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def test_cvt_exhaustive_nonnegative_below_464(probes):
+    hi = int(np.float32(464.0).view(np.uint32))
+    chunk = 1 << 26
+    out = torch.empty(chunk, dtype=torch.uint8, device="cuda")
+    for lo in range(0, hi, chunk):
+        n = min(chunk, hi - lo)
+        assert probes.probe_cvt_range(lo, n, out.data_ptr(), _stream()) == 0
+        got = out[:n].cpu().numpy()
+        want = oracle.e4m3_encode(np.arange(lo, lo + n, dtype=np.uint32).view(np.float32))
+        bad = np.nonzero(got != want)[0]
+        assert bad.size == 0, [(hex(lo + int(i)), int(got[i]), int(want[i])) for i in bad[:8]]
+
+
+def test_cvt_negative_and_specials(probes):
+    rng = np.random.default_rng(5)
+    neg = -np.abs(rng.standard_normal(1 << 20).astype(np.float32) * 50)
+    neg = neg[neg > -448]
+    x = np.concatenate([neg, np.float32([2.0 ** -10, 2.0 ** -9, 7.5 * 2.0 ** -9, 448, 0.0, -0.0])])
+    if x.size % 2:
+        x = np.append(x, np.float32(1.0))
+    xt = torch.from_numpy(x).cuda()
+    out = torch.empty(x.size, dtype=torch.uint8, device="cuda")
+    assert probes.probe_cvt_list(xt.data_ptr(), x.size, out.data_ptr(), 1.0, 0, 0, _stream()) == 0
+    assert np.array_equal(out.cpu().numpy(), oracle.e4m3_encode(x))
+    # the high-word form writes the same codes into bytes 2..3
+    assert probes.probe_cvt_list(xt.data_ptr(), x.size, out.data_ptr(), 1.0, 0, 1, _stream()) == 0
+    assert np.array_equal(out.cpu().numpy(), oracle.e4m3_encode(x))
+
+
+@pytest.mark.parametrize("k", [0, 4, 8])
+def test_scaled_cvt_equals_cvt_of_scaled(probes, k):
+    rng = np.random.default_rng(6 + k)
+    P = np.concatenate([rng.uniform(0, 1, 1 << 20), np.exp2(rng.uniform(-40, 0, 1 << 20)),
+                        2.0 ** -np.arange(0, 40), [1.0, 0.0]]).astype(np.float32)
+    if P.size % 2:
+        P = np.append(P, np.float32(0.5))
+    S = np.float32(2.0 ** k)
+    Pt = torch.from_numpy(P).cuda()
+    out = torch.empty(P.size, dtype=torch.uint8, device="cuda")
+    for hi in (0, 1):
+        assert probes.probe_cvt_list(Pt.data_ptr(), P.size, out.data_ptr(), float(1 / S), 1, hi, _stream()) == 0
+        assert np.array_equal(out.cpu().numpy(), oracle.e4m3_encode(P * S)), hi
+
+
+def test_exp2_exact_at_integers_and_monotone(probes):
+    """For S = 2^k the zero-code threshold is x = -(10 + k); with |x| >= 8 one
+    FP32 step of x moves 2^x by more than 5 ulps, so the hardware result must
+    sit strictly on the correct side of 2^n for every neighbour of n."""
+    ints = np.arange(-126, 1, dtype=np.float32)
+    nb = []
+    for n in range(-40, -7):
+        c = np.float32(n).view(np.uint32)
+        # negative floats: a larger bit pattern is more negative
+        nb.append(np.arange(c - 256, c + 257, dtype=np.uint32).view(np.float32))
+    x = np.concatenate([ints] + nb).astype(np.float32)
+    xt = torch.from_numpy(x).cuda()
+    out = torch.empty_like(xt)
+    assert probes.probe_exp2(xt.data_ptr(), x.size, out.data_ptr(), _stream()) == 0
+    y = out.cpu().numpy().astype(np.float64)
+    xi = x.astype(np.float64)
+    assert np.array_equal(y[:ints.size], np.exp2(ints.astype(np.float64)))
+    rest_x, rest_y = xi[ints.size:], y[ints.size:]
+    n = np.round(rest_x)
+    below, above = rest_x < n, rest_x > n
+    assert np.all(rest_y[below] < np.exp2(n[below]))
+    assert np.all(rest_y[above] > np.exp2(n[above]))
+
+
+def test_exp2_accuracy(probes):
+    rng = np.random.default_rng(7)
+    x = rng.uniform(-60, 0.001, 1 << 22).astype(np.float32)
+    xt = torch.from_numpy(x).cuda()
+    out = torch.empty_like(xt)
+    assert probes.probe_exp2(xt.data_ptr(), x.size, out.data_ptr(), _stream()) == 0
+    y = out.cpu().numpy()
+    ref = np.exp2(x.astype(np.float64))
+    ulp = np.spacing(ref.astype(np.float32)).astype(np.float64)
+    err = np.abs(y.astype(np.float64) - ref) / ulp
+    assert err.max() <= 2.0, err.max()
+
+
+def test_mfma_bf16_layout(probes):
+    rng = np.random.default_rng(8)
+    A = rng.integers(-8, 9, (32, 16)).astype(np.float32)
+    B = rng.integers(-8, 9, (16, 32)).astype(np.float32)
+    At = torch.from_numpy(A).to(torch.bfloat16).cuda()
+    Bt = torch.from_numpy(B).to(torch.bfloat16).cuda()
+    D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+    assert probes.probe_mfma(0, At.data_ptr(), Bt.data_ptr(), D.data_ptr(), _stream()) == 0
+    assert np.array_equal(D.cpu().numpy(), A @ B)
+
+
+def test_mfma_fp8_layout(probes):
+    rng = np.random.default_rng(9)
+    A = rng.integers(-8, 9, (32, 64)).astype(np.float32) / 4
+    B = rng.integers(-8, 9, (64, 32)).astype(np.float32) / 8
+    Ac = torch.from_numpy(A).to(torch.float8_e4m3fn).view(torch.uint8).cuda()
+    Bc = torch.from_numpy(B).to(torch.float8_e4m3fn).view(torch.uint8).cuda()
+    D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+    assert probes.probe_mfma(1, Ac.data_ptr(), Bc.data_ptr(), D.data_ptr(), _stream()) == 0
+    assert np.array_equal(D.cpu().numpy(), A @ B)
+
+
+def test_mfma_f32_layout(probes):
+    rng = np.random.default_rng(10)
+    A = rng.integers(-8, 9, (32, 2)).astype(np.float32)
+    B = rng.integers(-8, 9, (2, 32)).astype(np.float32)
+    At, Bt = torch.from_numpy(A).cuda(), torch.from_numpy(B).cuda()
+    D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+    assert probes.probe_mfma(2, At.data_ptr(), Bt.data_ptr(), D.data_ptr(), _stream()) == 0
+    assert np.array_equal(D.cpu().numpy(), A @ B)
