@@ -1,0 +1,274 @@
+"""Throughput benchmark of the FP8 attention forward on one MI355X.
+
+One step = one attn_fp8_fwd call over the whole workload (every query row of
+every batch and head: QK^T, online softmax over the KV blocks in the chosen
+order, E4M3 P-cast, P.V, epilogue).  Inputs are seeded synthetic sink-shaped
+tensors already resident in HBM when the timed region starts.
+
+Prints ONE JSON line:
+  value      whole-job TFLOP/s (FlashAttention convention 4*B*H*N^2*d, halved
+             under causal masking) over K timed steps bracketed by device syncs;
+  roofline   the attention kernel's algorithmic FLOPs per launch divided by its
+             average launch time from HIP events on its stream, against the
+             dense FP8 MFMA peak (and, for reference, the mixed bf16+FP8 peak
+             this kernel's instruction mix can reach);
+  cpu_baseline  the CPU oracle timed on a bounded row sample of the same
+             workload (rank 0 only), plus the P-cast MSE of the GPU and of the
+             oracle against FP64 attention on those rows.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"fp8": 5000.0, "bf16": 2500.0}
+# half of the FLOPs (QK^T) run on the bf16 MFMA, half (P.V) on the FP8 MFMA
+MIXED_PEAK = 2.0 / (1.0 / PEAK_TFLOPS["bf16"] + 1.0 / PEAK_TFLOPS["fp8"])
+KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast.hip", "paper_2606_06521_amd/csrc/attn_common.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fast_kernel_causal_mha_b4_h32_n8192_d128.json")
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, only
+    if it was taken on the current kernel source and this workload."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash() or t.get("workload") != workload:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--order", default=None, choices=[None, "forward", "reverse"])
+    ap.add_argument("--S", type=float, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="also run one device copy of this size (for counter calibration)")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two rocprofv3 --pmc counter CSVs (FETCH_SIZE, WRITE_SIZE) of a "
+                         "run with --copy-calibration-mib into the traffic summary and exit")
+    return ap.parse_args()
+
+
+def write_traffic(fetch_csv: str, write_csv: str, workload: str, copy_mib: int = 1024) -> dict:
+    """HBM bytes per launch of the fast kernel from the two counter passes.
+    Each counter is scaled by bytes_copied / counter_reading of the largest
+    device copy in the same run (a plain copy of ``copy_mib`` MiB)."""
+    import csv
+
+    def read(path):
+        rows = list(csv.DictReader(open(path)))
+        kern = [float(r["Counter_Value"]) for r in rows if "fast_kernel" in r["Kernel_Name"]
+                and "true, false" in r["Kernel_Name"]]
+        copy = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
+        return sum(kern) / len(kern), copy
+
+    f_kib, f_copy = read(fetch_csv)
+    w_kib, w_copy = read(write_csv)
+    true_kib = copy_mib * 1024.0
+    f_scale, w_scale = true_kib / f_copy, true_kib / w_copy
+    t = {
+        "workload": workload,
+        "kernel_source_sha256": kernel_source_hash(),
+        "fetch_kib_per_launch_raw": f_kib,
+        "write_kib_per_launch_raw": w_kib,
+        "copy_calibration_mib": copy_mib,
+        "fetch_scale": f_scale,
+        "write_scale": w_scale,
+        "hbm_read_bytes_per_launch": f_kib * 1024 * f_scale,
+        "hbm_write_bytes_per_launch": w_kib * 1024 * w_scale,
+        "hbm_bytes_per_launch": f_kib * 1024 * f_scale + w_kib * 1024 * w_scale,
+    }
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(t, f, indent=1)
+    return t
+
+
+def main() -> int:
+    args = parse()
+    if args.write_traffic:
+        from paper_2606_06521_amd.workloads import HEADLINE
+        print(json.dumps(write_traffic(*args.write_traffic, args.workload or HEADLINE)))
+        return 0
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build runs on one GPU only; the path shards over (batch, KV-head) "
+              "groups with no communication, so multi-GPU throughput is not measured here.",
+              file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2606_06521_amd import attn_fp8 as A
+    from paper_2606_06521_amd.inputs import make_inputs, sample_rows
+    from paper_2606_06521_amd.workloads import HEADLINE, WORKLOADS
+
+    w = WORKLOADS[args.workload or HEADLINE]
+    order = args.order or w.orders[-1]
+    S = args.S or w.scales[-1]
+    delta = w.deltas[0]
+    torch.cuda.set_device(0)
+    t_gen = time.time()
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=delta, seed=w.seed_base,
+                      bias_var=w.bias_var)
+    if w.fmt == "f32":
+        q = torch.from_numpy(inp.q_dev).cuda()
+        k = torch.from_numpy(inp.k_dev).cuda()
+        v = torch.from_numpy(inp.v_dev).cuda()
+    else:
+        q = torch.from_numpy(inp.q_dev.view(np.int16)).cuda().view(torch.bfloat16)
+        k = torch.from_numpy(inp.k_dev.view(np.int16)).cuda().view(torch.bfloat16)
+        v = torch.from_numpy(inp.v_dev).cuda().view(torch.float8_e4m3fn)
+    out = torch.empty((w.B, w.Hq, w.N, w.d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device="cuda")
+    gen_s = time.time() - t_gen
+
+    if args.copy_calibration_mib > 0:
+        src = torch.empty(args.copy_calibration_mib << 18, dtype=torch.float32, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    stream = torch.cuda.current_stream()
+    sptr = stream.cuda_stream
+    mode = A.MODES[w.mode]
+    ordc = A.ORDERS[order]
+    ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr())
+
+    def step():
+        st = A.attn_fp8_fwd(*ptrs, w.B, w.Hq, w.Hkv, w.N, w.d, int(w.causal), w.block_kv, ordc, S,
+                            mode, sptr)
+        if st != A.ATTN_OK:
+            raise A.AttnError(st)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for s_ev, e_ev in ev:
+        s_ev.record(stream)
+        step()
+        e_ev.record(stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kernel_ms = [s_ev.elapsed_time(e_ev) for s_ev, e_ev in ev]
+    kernel_ms_avg = float(np.mean(kernel_ms))
+    flops = w.flops()
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    achieved = flops / (kernel_ms_avg * 1e-3) / 1e12
+
+    # P-underflow diagnostic on the same inputs (timed separately, not reported as throughput)
+    cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=w.causal, block_kv=w.block_kv,
+                              mode=w.mode, n_sink=inp.n_sink)
+    torch.cuda.synchronize()
+    cnt_np = cnt.cpu().numpy().view(np.uint32).reshape(-1, 3)
+    counts_total = [int(x) for x in cnt_np.sum(0, dtype=np.uint64)]
+
+    res = {
+        "metric": "FP8-attn fwd TFLOP/s (% MFMA peak) at N=8192 d=128; P-cast MSE vs FP64",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 QK^T + e4m3 P.V, fp32 accumulate" if w.mode == "fast" else "fp32",
+        "data": "synthetic (seeded sink workload, Delta=%g, 4 sink keys)" % delta,
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
+                   "causal": w.causal, "mode": w.mode, "block_kv": w.block_kv, "order": order,
+                   "S": S, "delta_eff": round(inp.delta_eff, 4), "parallelism": "single GPU"},
+        "roofline": {
+            "bound": "mfma",
+            "achieved": round(achieved, 2),
+            "peak": PEAK_TFLOPS["fp8"] if w.mode == "fast" else 157.3,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / (PEAK_TFLOPS["fp8"] if w.mode == "fast" else 157.3), 4),
+            "traffic": measured_traffic(w.name),
+            "kernel_ms_avg": round(kernel_ms_avg, 4),
+            "flops_per_launch": flops,
+            "mixed_bf16_fp8_peak": round(MIXED_PEAK, 1) if w.mode == "fast" else None,
+            "frac_of_mixed_peak": round(achieved / MIXED_PEAK, 4) if w.mode == "fast" else None,
+        },
+        "p_underflow_counts": {"sink": counts_total[0], "sink_block_nonsink": counts_total[1],
+                               "other_blocks": counts_total[2]},
+        "input_gen_s": round(gen_s, 2),
+    }
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(inp, w, order, S, out, cnt_np, sample_rows)
+    print(json.dumps(res), flush=True)
+    return 0
+
+
+def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows):
+    """The oracle (as it stands) on a bounded row sample of the same workload,
+    plus P-cast MSE of the GPU output and of the oracle against FP64 attention."""
+    import numpy as np
+
+    import oracle
+
+    nthreads = min(16, oracle.default_threads())
+    every = max(1, (w.B * w.Hq * w.N) // 32768)
+    rows = np.arange(0, w.B * w.Hq * w.N, every, dtype=np.int64)
+    rows = np.unique(np.concatenate([rows, sample_rows(w.B, w.Hq, w.N, 128, 10 ** 9, seed=0)[:64]]))
+    keys = (rows % w.N + 1) if w.causal else np.full(rows.size, w.N)
+    flops = float(4.0 * w.d * keys.sum())
+    t0 = time.perf_counter()
+    o_out, o_lse, o_cnt = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,
+                                      block_kv=w.block_kv, causal=w.causal, n_sink=inp.n_sink,
+                                      rows=rows, nthreads=nthreads)
+    dt = time.perf_counter() - t0
+    ref, _ = oracle.ref_fp64(inp.q32, inp.k32, inp.v32, causal=w.causal, rows=rows, nthreads=nthreads)
+    g = out_dev.cpu().numpy().reshape(-1, w.d)[rows]
+    mse_gpu = float(np.mean((g.astype(np.float64) - ref) ** 2))
+    mse_oracle = float(np.mean((o_out.astype(np.float64) - ref) ** 2))
+    return {
+        "value": round(flops / dt / 1e12, 6),
+        "unit": "TFLOP/s",
+        "cores": nthreads,
+        "kind": "oracle",
+        "sample": f"{rows.size} query rows (every {every}th flat row of all batches/heads, "
+                  f"{int(keys.sum())} (row, key) pairs, {flops:.3e} FLOP) in {dt:.2f} s",
+        "oracle_s": round(dt, 3),
+        "mse_gpu_vs_fp64": mse_gpu,
+        "mse_oracle_vs_fp64": mse_oracle,
+        "max_abs_gpu_minus_oracle": float(np.abs(g - o_out).max()),
+        "counts_equal_on_sample": bool(np.array_equal(cnt_gpu[rows], o_cnt)),
+    }
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -61,10 +61,12 @@ def lib() -> ctypes.CDLL:
 
 
 def default_threads() -> int:
+    """Usable host cores, capped at 16 (the CPU share of one GPU on the GPU hosts)."""
     try:
-        return max(1, len(os.sched_getaffinity(0)))
+        n = len(os.sched_getaffinity(0))
     except AttributeError:  # pragma: no cover
-        return max(1, os.cpu_count() or 1)
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def _ptr(a: np.ndarray | None):
