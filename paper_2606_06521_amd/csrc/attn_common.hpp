@@ -88,6 +88,22 @@ __device__ inline uint32_t other_half_u32(uint32_t x)
     return (uint32_t)__shfl_xor((int)x, 32, 64);
 }
 
+// max / sum of a value over the two 32-lane halves (lane i and lane i ^ 32),
+// returned in every lane.  v_permlane32_swap with both operands x yields the
+// lower-half values and the upper-half values, each in all 64 lanes; the
+// symmetric combine does not depend on which result holds which half.
+__device__ inline float halves_max(float x)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ inline float halves_sum(float x)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ inline float fmax_f(float a, float b) { return __builtin_fmaxf(a, b); }
 
 // Number of zero bytes in a 32-bit word.

@@ -1,8 +1,7 @@
 // Fast mode: bfloat16 Q and K, OCP E4M3 V; the E4M3 P bytes feed the FP8 MFMA.
 //
-// Algorithm 1 per query row with the kernel semantics of Sec. 6.1; NW waves of
-// 32 query rows per workgroup (BM = 32*NW rows), one KV block of BC keys per
-// iteration, in forward or reverse block order:
+// Algorithm 1 per query row with the kernel semantics of Sec. 6.1, one KV block
+// of BC keys per iteration, in forward or reverse block order:
 //   S^T = K_j Q^T        v_mfma_f32_32x32x16_bf16, FP32 accumulate (raw dots)
 //   m, alpha, P, l       per-lane scalars (one query row per lane)
 //   P8 = E4M3(P * S)     v_cvt_pk_fp8_f32 (round to nearest even); for S = 2^k
@@ -10,11 +9,22 @@
 //                        the exact power-of-two scale inside the convert
 //   O^T += V_j^T P8^T    v_mfma_f32_32x32x64_f8f6f4 (E4M3 x E4M3), FP32 accumulate
 //   out = O / (S l)
-// K_j / V_j go global -> registers (prefetched one block ahead) -> LDS.  V_j is
-// transposed on the way (4x4 byte transposes with v_perm_b32) into a
-// d-major layout, because both operands of the FP8 MFMA need the key index
-// contiguous per lane.  Both LDS tiles are XOR-swizzled so the MFMA operand
-// reads (16 bytes per lane) hit distinct banks.
+//
+// Schedule ("ping-pong"): 8 waves of 32 query rows; waves w and w+4 share a
+// SIMD.  Group 0 (waves 0-3) and group 1 (waves 4-7) alternate between an MFMA
+// phase (P.V of the previous block, then S^T of the current block) and a VALU
+// phase (max, exp2, l, cast, rescale of O), one phase apart, with a workgroup
+// barrier between phases.  On every SIMD one wave keeps the matrix core busy
+// while the other runs the softmax.
+//
+// K_j and V_j go global -> LDS with no register staging
+// (global_load_lds_dwordx4, lane i -> LDS base + 16 i), double-buffered, issued
+// by group 0 at the start of its MFMA phase two phases before first use.
+// K rows are stored in the order the S^T MFMA reads them (a key permutation
+// inside each 32-key tile, see a_row_to_key); V stays key-major and is read
+// transposed by ds_read_b64_tr_b8, which hands each lane 8 consecutive keys of
+// its d column.  Rows are padded by 16 bytes so the 16-byte (K) and 8-byte
+// transposed (V) reads of a 16-lane group fall in distinct banks.
 #include "attn_common.hpp"
 #include "attn_launch.hpp"
 
@@ -24,59 +34,57 @@ namespace attn {
 
 namespace {
 
-// 16-byte chunk swizzle of a K row (key kappa): the eight keys that lanes
-// 0..7 (and 8..15, ...) of a wave read together map to eight different chunks.
-__device__ inline int k_swz(int key)
+typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+
+// One 16-byte-per-lane direct load: lane i writes LDS bytes [dst + 16 i, +16).
+// Issued as inline assembly so the compiler does not tie its completion to
+// the next barrier; the kernel waits for it explicitly (wait_loads) before
+// the barrier that publishes the stage.  M0 holds the wave's LDS base and is
+// used by nothing else in this kernel.
+__device__ inline void g2lds16(const void* src, void* dst_wave_base)
 {
-    return (key & 3) | (((key >> 4) & 1) << 2);
+    const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)dst_wave_base;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(src)
+                 : "memory");
 }
 
-// 16-byte chunk swizzle of a V^T row (d index).
-template <int BC>
-__device__ inline int v_swz(int d)
+__device__ inline void wait_loads()
 {
-    if constexpr (BC == 128)
-        return (d ^ (d >> 3)) & 7;
-    else
-        return (d >> 1) & 3;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Transpose a 4 (keys) x 4 (bytes) block: a[i] holds 4 consecutive d-bytes of
-// key i; out[e] holds byte e of keys 0..3 (key 0 in the low byte).
-__device__ inline void transpose4x4(const uint32_t a0, const uint32_t a1, const uint32_t a2,
-                                    const uint32_t a3, uint32_t out[4])
+__device__ inline i32x2 lds_read_tr8(const uint8_t* p)
 {
-    const uint32_t t0 = __builtin_amdgcn_perm(a1, a0, 0x05010400u);
-    const uint32_t t1 = __builtin_amdgcn_perm(a1, a0, 0x07030602u);
-    const uint32_t t2 = __builtin_amdgcn_perm(a3, a2, 0x05010400u);
-    const uint32_t t3 = __builtin_amdgcn_perm(a3, a2, 0x07030602u);
-    out[0] = __builtin_amdgcn_perm(t2, t0, 0x05040100u);
-    out[1] = __builtin_amdgcn_perm(t2, t0, 0x07060302u);
-    out[2] = __builtin_amdgcn_perm(t3, t1, 0x05040100u);
-    out[3] = __builtin_amdgcn_perm(t3, t1, 0x07060302u);
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) i32x2*)(p));
 }
 
 }  // namespace
 
-template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2, int NW>
-__global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
+template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2>
+__global__ void __launch_bounds__(512) fast_kernel(Params p)
 {
+    constexpr int NW = 8;
     constexpr int BM = 32 * NW;
-    constexpr int NT = NW * 64;
     constexpr int KT = BC / 32;                 // 32-key S^T tiles per block
     constexpr int DK = D / 16;                  // bf16 MFMA k-steps over d
     constexpr int DT = D / 32;                  // 32-wide d tiles of O^T
     constexpr int PVS = BC / 64;                // 64-key FP8 MFMA k-steps
-    constexpr int KROW = D * 2;                 // bytes per K row
-    constexpr int KCH = D / 8;                  // 16-byte chunks per K row
-    constexpr int K_UNITS = BC * KCH;
-    constexpr int K_PER_T = (K_UNITS + NT - 1) / NT;
-    constexpr int V_UNITS = (BC / 4) * (D / 8); // units of 4 keys x 8 d-bytes
-    constexpr int V_PER_T = (V_UNITS + NT - 1) / NT;
-    static_assert(KCH >= 8, "K swizzle needs at least 8 chunks per row");
+    constexpr int KROW = D * 2;                 // bytes per K row in HBM
+    constexpr int KS = KROW + 16;               // K row stride in LDS (padded)
+    constexpr int VS = D + 16;                  // V row stride in LDS (padded)
+    constexpr int KCHR = KS / 16;               // 16-byte chunks per LDS K row (last = pad)
+    constexpr int VCHR = VS / 16;
+    constexpr int K_CH = BC * KCHR;             // chunks per K stage
+    constexpr int V_CH = BC * VCHR;
+    constexpr int K_BYTES = K_CH * 16;
+    constexpr int V_BYTES = V_CH * 16;
 
-    __shared__ __attribute__((aligned(16))) uint8_t Ks[BC * KROW];
-    __shared__ __attribute__((aligned(16))) uint8_t Vt[D * BC];
+    __shared__ __attribute__((aligned(16))) uint8_t Ks0[K_BYTES];
+    __shared__ __attribute__((aligned(16))) uint8_t Ks1[K_BYTES];
+    __shared__ __attribute__((aligned(16))) uint8_t Vs0[V_BYTES];
+    __shared__ __attribute__((aligned(16))) uint8_t Vs1[V_BYTES];
 
     int bh, tile;
     if (!map_tile<CAUSAL>(p, bh, tile))
@@ -87,7 +95,8 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
     const int hk = hq / (p.Hq / p.Hkv);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, scalar
+    const int grp = w >> 2;                                   // 0: waves 0-3, 1: waves 4-7
     const int n = lane & 31;
     const int h = lane >> 5;
     const int row0 = tile * BM;
@@ -98,6 +107,42 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
     const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)N;
     const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
     const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * D;
+
+    const int last_row_wg = min(row0 + BM, N) - 1;
+    const int nb = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
+    const bool wave_on = wrow0 < N;
+    // every row of a wave lies in one BC-block of rows (BC is a multiple of 32)
+    const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nb;
+    auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
+    auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
+
+    // ---- direct global -> LDS loads of one K / V stage ----
+    // LDS chunk c of a K stage is row c / KCHR (LDS row r holds key
+    // 32 (r/32) + a_row_to_key(r % 32)), 16-byte chunk c % KCHR (the last chunk
+    // of a row is padding).  Keys past the end of the sequence read row N-1:
+    // they are masked to P = 0 before they can contribute.
+    auto load_k = [&](uint8_t* dst, int j, int t_first, int t_count) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        for (int c0 = t_first * 64; c0 < K_CH; c0 += t_count * 64) {
+            const int c = c0 + lane;
+            const int r = c / KCHR;
+            int ch = c - r * KCHR;
+            ch = ch == KCHR - 1 ? 0 : ch;
+            const int key = min(t0 + 32 * (r >> 5) + a_row_to_key(r & 31), N - 1);
+            g2lds16(Kg + (size_t)key * KROW + ch * 16, dst + c0 * 16);
+        }
+    };
+    auto load_v = [&](uint8_t* dst, int j, int t_first, int t_count) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        for (int c0 = t_first * 64; c0 < V_CH; c0 += t_count * 64) {
+            const int c = c0 + lane;
+            const int r = c / VCHR;
+            int ch = c - r * VCHR;
+            ch = ch == VCHR - 1 ? 0 : ch;
+            const int key = min(t0 + r, N - 1);
+            g2lds16(Vg + (size_t)key * D + ch * 16, dst + c0 * 16);
+        }
+    };
 
     // Q^T fragments (B operand): lane (n, h) holds Q[row][16*kk + 8*h .. +8]
     bf16x8 qf[DK];
@@ -114,77 +159,10 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
                 qf[kk][i] = (__bf16)0.f;
     }
 
-    const int last_row_wg = min(row0 + BM, N) - 1;
-    const int nblk = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
-    const bool wave_on = wrow0 < N;
-    const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nblk;
-    const int a_key = a_row_to_key(n);
-    const int a_swz = k_swz(a_key);              // same for every 32-key tile
-
-    // ---- global -> register prefetch of one KV block ----
-    i32x4 kreg[K_PER_T];
-    uint32_t vreg[V_PER_T][8];                   // 4 keys x (lo, hi) dwords
-    auto load_block = [&](int j) {
-        const int t0 = j * BC;
-#pragma unroll
-        for (int i = 0; i < K_PER_T; ++i) {
-            const int u = tid + i * NT;
-            if (K_UNITS % NT == 0 || u < K_UNITS) {
-                const int key = u / KCH;
-                const int ch = u - key * KCH;
-                if (t0 + key < N)
-                    kreg[i] = *reinterpret_cast<const i32x4*>(Kg + (size_t)(t0 + key) * KROW + ch * 16);
-                else
-                    kreg[i] = i32x4{0, 0, 0, 0};
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < V_PER_T; ++i) {
-            const int u = tid + i * NT;
-            if (V_UNITS % NT == 0 || u < V_UNITS) {
-                const int kg = u / (D / 8);
-                const int dc = u - kg * (D / 8);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int key = t0 + 4 * kg + e;
-                    i32x2 t = {0, 0};
-                    if (key < N)
-                        t = *reinterpret_cast<const i32x2*>(Vg + (size_t)key * D + dc * 8);
-                    vreg[i][2 * e] = (uint32_t)t[0];
-                    vreg[i][2 * e + 1] = (uint32_t)t[1];
-                }
-            }
-        }
-    };
-    auto store_block = [&]() {
-#pragma unroll
-        for (int i = 0; i < K_PER_T; ++i) {
-            const int u = tid + i * NT;
-            if (K_UNITS % NT == 0 || u < K_UNITS) {
-                const int key = u / KCH;
-                const int ch = u - key * KCH;
-                *reinterpret_cast<i32x4*>(Ks + key * KROW + ((ch ^ k_swz(key)) << 4)) = kreg[i];
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < V_PER_T; ++i) {
-            const int u = tid + i * NT;
-            if (V_UNITS % NT == 0 || u < V_UNITS) {
-                const int kg = u / (D / 8);
-                const int dc = u - kg * (D / 8);
-                uint32_t tl[4], th[4];
-                transpose4x4(vreg[i][0], vreg[i][2], vreg[i][4], vreg[i][6], tl);
-                transpose4x4(vreg[i][1], vreg[i][3], vreg[i][5], vreg[i][7], th);
-                const int kb = 4 * kg;               // first key (byte) of the unit
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int d = 8 * dc + e;
-                    const int off = d * BC + ((((kb >> 4) ^ v_swz<BC>(d))) << 4) + (kb & 15);
-                    *reinterpret_cast<uint32_t*>(Vt + off) = e < 4 ? tl[e] : th[e - 4];
-                }
-            }
-        }
-    };
+    // per-lane LDS offsets; every fragment read is base + an immediate
+    const int k_lane = n * KS + 16 * h;                       // S^T A operand: LDS row n, chunk 2kk + h
+    const int j16 = n & 15;                                   // lane within its 16-lane group
+    const int v_lane = ((j16 >> 1) + 16 * h) * VS + 16 * (n >> 4) + 8 * (j16 & 1);
 
     const float c = p.c;
     const float S = p.S;
@@ -198,86 +176,181 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
 #pragma unroll
         for (int r = 0; r < 16; ++r)
             o[dt][r] = 0.f;
+    f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
+    uint32_t pk[KT][4];           // E4M3 P bytes between the VALU and the next MFMA phase
     uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
 
-    load_block(p.order == 0 ? 0 : nblk - 1);
-    for (int it = 0; it < nblk; ++it) {
-        const int j = (p.order == 0) ? it : nblk - 1 - it;
-        const int t0 = j * BC;
-        __syncthreads();                 // previous block fully consumed
-        store_block();
-        if (it + 1 < nblk)
-            load_block(p.order == 0 ? it + 1 : nblk - 2 - it);
-        __syncthreads();                 // block j resident in LDS
-        if (!wave_on || j >= nblk_w)
-            continue;
+    // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
+    // The K fragments of k-step kk+1 are requested before the four MFMAs of
+    // step kk are issued (two register sets), so the LDS latency overlaps the
+    // matrix core instead of stalling every MFMA; sched_barrier keeps the
+    // compiler from sinking the reads back next to their uses.
+    auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
+        const uint8_t* kb = kst + k_lane;
+        bf16x8 a0[KT], a1[KT];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+            a0[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS);
+#pragma unroll
+        for (int kk = 0; kk < DK; kk += 2) {
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+                a1[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS + (kk + 1) * 32);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                if (kk == 0)
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kt], qf[kk], f32x16{}, 0, 0, 0);
+                else
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kt], qf[kk], s[kt], 0, 0, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (kk + 2 < DK) {
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+                    a0[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS + (kk + 2) * 32);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kt], qf[kk + 1], s[kt], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    };
 
-        // ---- S^T = K_j Q^T ----
-        f32x16 s[KT];
+    // ---- O^T += V_j^T P8^T ----
+    // V^T operands of the next MFMA are read (transposed) while the current
+    // one runs.
+    auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
+        const uint8_t* vb = vst + v_lane;
+        auto vload = [&](int js, int dt) __attribute__((always_inline)) {
+            const uint8_t* va = vb + 32 * dt + 64 * js * VS;
+            const i32x2 r0 = lds_read_tr8(va);
+            const i32x2 r1 = lds_read_tr8(va + 8 * VS);
+            const i32x2 r2 = lds_read_tr8(va + 32 * VS);
+            const i32x2 r3 = lds_read_tr8(va + 40 * VS);
+            return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+        };
+        i32x8 anext = vload(0, 0);
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) {
+        for (int js = 0; js < PVS; ++js) {
+            i32x8 bop;
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                s[kt][r] = 0.f;
-            const uint8_t* krow = Ks + (32 * kt + a_key) * KROW;
+            for (int q4 = 0; q4 < 4; ++q4) {
+                bop[q4] = (int)pk[2 * js][q4];
+                bop[4 + q4] = (int)pk[2 * js + 1][q4];
+            }
 #pragma unroll
-            for (int kk = 0; kk < DK; ++kk) {
-                const int ch = 2 * kk + h;
-                const bf16x8 a = *reinterpret_cast<const bf16x8*>(krow + ((ch ^ a_swz) << 4));
-                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], s[kt], 0, 0, 0);
+            for (int dt = 0; dt < DT; ++dt) {
+                const i32x8 aop = anext;
+                if (dt + 1 < DT)
+                    anext = vload(js, dt + 1);
+                else if (js + 1 < PVS)
+                    anext = vload(js + 1, 0);
+                __builtin_amdgcn_sched_barrier(0);
+                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(aop, bop, o[dt], 0, 0, 0, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
+    };
 
-        // ---- mask: keys past the end of the sequence, keys after the row ----
+    // ---- running max, alpha, P, l (pre-cast), E4M3 cast, rescale of O ----
+    auto softmax = [&](int j) __attribute__((always_inline)) {
+        const int t0 = j * BC;
         if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
+            // key t0 + 32 kt + 16 h + r is valid iff 32 kt + r <= lim; masked
+            // scores become -inf through a sign-mask bit select (no compares)
+            const int lim = (CAUSAL ? min(row, N - 1) : N - 1) - t0 - 16 * h;
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int key = t0 + 32 * kt + 16 * h + r;
-                    if (key >= N || (CAUSAL && key > row))
-                        s[kt][r] = -INFINITY;
+                    const uint32_t m = (uint32_t)((lim - (32 * kt + r)) >> 31);
+                    const float sv = s[kt][r];
+                    const uint32_t x = __float_as_uint(sv);
+                    s[kt][r] = __uint_as_float((x & ~m) | (0xFF800000u & m));
                 }
         }
-
-        // ---- running max, alpha ----
-        float mx = -INFINITY;
+        // row maximum: one independent chain per 32-key tile, then the tiles,
+        // then the two lane halves (a maximum is exact in any order)
+        float mk[KT];
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
+        for (int kt = 0; kt < KT; ++kt) {
+            float a = s[kt][0];
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                mx = fmax_f(mx, s[kt][r]);
-        mx = fmax_f(mx, other_half(mx));
+            for (int r = 1; r < 16; ++r)
+                a = fmax_f(a, s[kt][r]);
+            mk[kt] = a;
+        }
+        float mx = mk[0];
+#pragma unroll
+        for (int kt = 1; kt < KT; ++kt)
+            mx = fmax_f(mx, mk[kt]);
+        mx = halves_max(mx);
         const float m_new = fmax_f(m_run, mx);
         const float mc_new = m_new * c;
         const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
         const float nmc = -mc_new;
-
-        // ---- P, l (pre-cast), E4M3 cast into the B operand of the P.V MFMA ----
-        float lsum = 0.f;
-        uint32_t pk[KT][4];
+        // The rest is organised in stages so that no instruction waits on the
+        // result of the one just before it (this phase runs alone on its
+        // SIMD's vector ALU while the partner wave drives the matrix core):
+        // (1) x = fma(D, c, -mc) for all keys, in place;
+        // (2) P = exp2(x) for all keys, in place, interleaved with the rescale
+        //     of O (independent work for the vector ALU while exp2 is in flight);
+        // (3) l from the pre-cast P (one partial sum per tile), E4M3 cast.
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                s[kt][r] = __builtin_fmaf(s[kt][r], c, nmc);
+        __builtin_amdgcn_sched_barrier(0);
+        // rescale O before this block's P.V; skipped when no row of the wave
+        // moved its maximum (alpha is then exactly 1)
+        const bool rescale = __ballot(alpha != 1.0f) != 0;
+        if (rescale) {
+#pragma unroll
+            for (int t = 0; t < DT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    o[t][r] *= alpha;
+        }
+        {
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        float lpart[KT];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+            float l0 = s[kt][0] + s[kt][1], l1 = s[kt][2] + s[kt][3];
+#pragma unroll
+            for (int r = 4; r < 16; r += 4) {
+                l0 += s[kt][r] + s[kt][r + 1];
+                l1 += s[kt][r + 2] + s[kt][r + 3];
+            }
+            lpart[kt] = l0 + l1;
+        }
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) {
 #pragma unroll
             for (int r4 = 0; r4 < 4; ++r4) {
-                float pv[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pv[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][4 * r4 + i], c, nmc));
-                    lsum += pv[i];
-                }
+                const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
+                const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
                 uint32_t word;
                 if constexpr (POW2) {
-                    typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+                    // (the first convert writes the low half, the second the high half)
                     s16x2 lo = {0, 0};
-                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, pv[0], pv[1], inv_S, false);
-                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, pv[2], pv[3], inv_S, true);
-                    word = __builtin_bit_cast(uint32_t, lo);
+                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, inv_S, false);
+                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, inv_S, true);
+                    word = ((uint32_t)(uint16_t)lo[1] << 16) | (uint32_t)(uint16_t)lo[0];
                 } else {
-                    const float y0 = __builtin_fminf(pv[0] * S, 448.f);
-                    const float y1 = __builtin_fminf(pv[1] * S, 448.f);
-                    const float y2 = __builtin_fminf(pv[2] * S, 448.f);
-                    const float y3 = __builtin_fminf(pv[3] * S, 448.f);
+                    const float y0 = __builtin_fminf(p0 * S, 448.f);
+                    const float y1 = __builtin_fminf(p1 * S, 448.f);
+                    const float y2 = __builtin_fminf(p2 * S, 448.f);
+                    const float y3 = __builtin_fminf(p3 * S, 448.f);
                     int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false);
                     wv = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, wv, true);
                     word = (uint32_t)wv;
@@ -298,36 +371,59 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
                 }
             }
         }
+        float lsum = lpart[0];
+#pragma unroll
+        for (int kt = 1; kt < KT; ++kt)
+            lsum += lpart[kt];
         ell = alpha * ell + lsum;
-
-        // ---- O <- alpha O + P8 V_j ----
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                o[dt][r] *= alpha;
-#pragma unroll
-        for (int js = 0; js < PVS; ++js) {
-            i32x8 bop;
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                bop[q4] = (int)pk[2 * js][q4];
-                bop[4 + q4] = (int)pk[2 * js + 1][q4];
-            }
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const int d = 32 * dt + n;
-                const uint8_t* vrow = Vt + d * BC;
-                const int sw = v_swz<BC>(d);
-                const i32x4 a0 = *reinterpret_cast<const i32x4*>(vrow + (((4 * js + h) ^ sw) << 4));
-                const i32x4 a1 = *reinterpret_cast<const i32x4*>(vrow + (((4 * js + 2 + h) ^ sw) << 4));
-                const i32x8 aop = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
-                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(aop, bop, o[dt], 0, 0, 0, 0, 0, 0);
-            }
-        }
         m_run = m_new;
         mc_run = mc_new;
+    };
+
+    // ---- prologue: K of the first block into stage 0 (all waves) ----
+    load_k(Ks0, jof(0), w, NW);
+    // Q fragments and the first K stage are complete after this point; the
+    // compiler sees the wait (it tracks no outstanding loads in the loop)
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    // Both groups run the same program -- per block k an MFMA phase (P.V of
+    // block k-1, S^T of block k) and a VALU phase (softmax of block k), each
+    // closed by a workgroup barrier -- but group 1 first passes one extra
+    // barrier, so it runs one phase behind group 0: while one wave of a SIMD
+    // is in its MFMA phase the other is in its softmax phase.  Group 0 issues
+    // the loads of K_{k+1} and V_k at the start of its MFMA phase k; they are
+    // first read two phases later.  Stage parity is k % 2 (the loop is
+    // unrolled twice so every LDS access names its stage statically).
+    if (grp == 1)
+        __syncthreads();
+    auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
+        __attribute__((always_inline)) {
+        if (grp == 0) {
+            if (k + 1 < nb)
+                load_k(k_nxt, jof(k + 1), w, 4);
+            if (k < nb)
+                load_v(v_cur, jof(k), w, 4);
+        }
+        if (valid(k - 1))
+            pv(v_prv);
+        if (valid(k))
+            qk(k_cur);
+        __syncthreads();
+        if (valid(k))
+            softmax(jof(k));
+        // the stage loads issued in the MFMA phase must land before the
+        // barrier that hands them to the next MFMA phase
+        if (grp == 0)
+            wait_loads();
+        __syncthreads();
+    };
+    for (int k = 0; k <= nb; k += 2) {
+        iteration(k, Ks0, Ks1, Vs0, Vs1);
+        if (k + 1 <= nb)
+            iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
     }
+    if (grp == 0)
+        __syncthreads();
 
     if (!wave_on)
         return;
@@ -366,16 +462,11 @@ __global__ void __launch_bounds__(NW * 64) fast_kernel(Params p)
     }
 }
 
-namespace {
-constexpr int kFastWaves = 4;
-}
-
 template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2>
 static hipError_t launch_one(const Params& p, hipStream_t stream)
 {
     const int grid = p.per_xcd * kNumXcd;
-    hipLaunchKernelGGL((fast_kernel<D, BC, CAUSAL, COUNT, POW2, kFastWaves>), dim3(grid),
-                       dim3(kFastWaves * 64), 0, stream, p);
+    hipLaunchKernelGGL((fast_kernel<D, BC, CAUSAL, COUNT, POW2>), dim3(grid), dim3(512), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -400,6 +491,6 @@ hipError_t launch_fast(const Params& p, int d, int block_kv, bool causal, bool c
                           : launch_d_bc<128, 128>(p, causal, count, pow2_scale, stream);
 }
 
-int fast_rows_per_wg(int, int) { return 32 * kFastWaves; }
+int fast_rows_per_wg(int, int) { return 256; }
 
 }  // namespace attn
