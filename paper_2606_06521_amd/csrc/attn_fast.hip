@@ -23,8 +23,11 @@
 // K rows are stored in the order the S^T MFMA reads them (a key permutation
 // inside each 32-key tile, see a_row_to_key); V stays key-major and is read
 // transposed by ds_read_b64_tr_b8, which hands each lane 8 consecutive keys of
-// its d column.  Rows are padded by 16 bytes so the 16-byte (K) and 8-byte
-// transposed (V) reads of a 16-lane group fall in distinct banks.
+// its d column.  Rows are unpadded; the 16-byte chunks of a row are permuted by
+// an XOR with a function of the row (kswz / vswz) so that the 16-byte K reads
+// and the transposed V reads of a lane group fall in distinct banks.  With
+// that layout a loading lane's HBM offset is a per-lane constant plus a
+// per-block scalar, so issuing a load costs no vector instructions.
 #include "attn_common.hpp"
 #include "attn_launch.hpp"
 
@@ -36,17 +39,18 @@ namespace {
 
 typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
 
-// One 16-byte-per-lane direct load: lane i writes LDS bytes [dst + 16 i, +16).
+// One 16-byte-per-lane direct load: lane i reads HBM bytes [base + voff, +16)
+// (base uniform, voff per lane) and writes LDS bytes [dst + 16 i, +16).
 // Issued as inline assembly so the compiler does not tie its completion to
 // the next barrier; the kernel waits for it explicitly (wait_loads) before
 // the barrier that publishes the stage.  M0 holds the wave's LDS base and is
 // used by nothing else in this kernel.
-__device__ inline void g2lds16(const void* src, void* dst_wave_base)
+__device__ inline void g2lds16(const uint8_t* base, uint32_t voff, const uint8_t* dst_wave_base)
 {
-    const uint32_t lds = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint8_t*)dst_wave_base;
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)dst_wave_base;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
-                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(src)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(base)
                  : "memory");
 }
 
@@ -71,20 +75,33 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     constexpr int DK = D / 16;                  // bf16 MFMA k-steps over d
     constexpr int DT = D / 32;                  // 32-wide d tiles of O^T
     constexpr int PVS = BC / 64;                // 64-key FP8 MFMA k-steps
-    constexpr int KROW = D * 2;                 // bytes per K row in HBM
-    constexpr int KS = KROW + 16;               // K row stride in LDS (padded)
-    constexpr int VS = D + 16;                  // V row stride in LDS (padded)
-    constexpr int KCHR = KS / 16;               // 16-byte chunks per LDS K row (last = pad)
-    constexpr int VCHR = VS / 16;
-    constexpr int K_CH = BC * KCHR;             // chunks per K stage
-    constexpr int V_CH = BC * VCHR;
-    constexpr int K_BYTES = K_CH * 16;
-    constexpr int V_BYTES = V_CH * 16;
+    constexpr int KROW = D * 2;                 // bytes per K row (HBM and LDS)
+    constexpr int VROW = D;                     // bytes per V row
+    constexpr int KCPR = KROW / 16;             // 16-byte chunks per row
+    constexpr int VCPR = VROW / 16;
+    constexpr int K_BYTES = BC * KROW;          // one K stage
+    constexpr int V_BYTES = BC * VROW;
+    constexpr int K_RPI = 1024 / KROW;          // rows written by one wave load instruction
+    constexpr int V_RPI = 1024 / VROW;
+    constexpr int K_NI = K_BYTES / 4096;        // load instructions per loading wave (4 waves)
+    constexpr int V_NI = V_BYTES / 4096;
+    static_assert(K_NI >= 1 && V_NI >= 1, "stage smaller than one round of loads");
 
-    __shared__ __attribute__((aligned(16))) uint8_t Ks0[K_BYTES];
-    __shared__ __attribute__((aligned(16))) uint8_t Ks1[K_BYTES];
-    __shared__ __attribute__((aligned(16))) uint8_t Vs0[V_BYTES];
-    __shared__ __attribute__((aligned(16))) uint8_t Vs1[V_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks0[K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks1[K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs0[V_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs1[V_BYTES];
+
+    // Chunk swizzles: LDS row r of a stage stores logical 16-byte chunk L at
+    // physical chunk L ^ swz(r).  kswz spreads the 16 rows read by a 16-lane
+    // group (one logical chunk) over the 16 bank slots of 256 bytes; vswz does
+    // the same for the 8 rows x 2 chunks read by a 32-lane transposed read.
+    // Both depend only on row bits below 5, so they are the same for every
+    // 32-row (K) or 8-row (V) translate of a row.
+    auto kswz = [](int r) __attribute__((always_inline)) { return (r / (256 / KROW)) & (KCPR - 1); };
+    auto vswz = [](int r) __attribute__((always_inline)) { return ((r / (256 / VROW)) & (VCPR / 2 - 1)) * 2; };
+    // LDS row of a K stage -> key offset in the block
+    auto krow_key = [](int r) __attribute__((always_inline)) { return 32 * (r >> 5) + a_row_to_key(r & 31); };
 
     int bh, tile;
     if (!map_tile<CAUSAL>(p, bh, tile))
@@ -116,31 +133,55 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
     auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
 
-    // ---- direct global -> LDS loads of one K / V stage ----
-    // LDS chunk c of a K stage is row c / KCHR (LDS row r holds key
-    // 32 (r/32) + a_row_to_key(r % 32)), 16-byte chunk c % KCHR (the last chunk
-    // of a row is padding).  Keys past the end of the sequence read row N-1:
-    // they are masked to P = 0 before they can contribute.
-    auto load_k = [&](uint8_t* dst, int j, int t_first, int t_count) __attribute__((always_inline)) {
+    // ---- direct global -> LDS loads of one K / V stage (waves 0-3) ----
+    // Load instruction i = wl + 4 it of a stage (wl = w & 3) writes LDS bytes
+    // [1024 i, +1024): lane l fills row 4 K_RPI it + rho, rho = wl K_RPI +
+    // l / KCPR, physical chunk l % KCPR, i.e. logical chunk
+    // (l % KCPR) ^ kswz(rho) of key krow_key(4 K_RPI it) + krow_key(rho)
+    // (4 K_RPI is a power of two >= 16, so the two key parts have disjoint
+    // bits and the swizzle does not depend on it).  V likewise with
+    // key = row.  Keys past the end of the sequence (only in a ragged last
+    // block) read row N-1: they are masked to P = 0 before they can contribute.
+    const int wl = w & 3;
+    int k_key_l, v_key_l;
+    uint32_t k_chunk_l, v_chunk_l;
+    {
+        const int rk = wl * K_RPI + lane / KCPR;
+        k_key_l = krow_key(rk);
+        k_chunk_l = (uint32_t)(((lane % KCPR) ^ kswz(rk)) * 16);
+        const int rv = wl * V_RPI + lane / VCPR;
+        v_key_l = rv;
+        v_chunk_l = (uint32_t)(((lane % VCPR) ^ vswz(rv)) * 16);
+    }
+    const uint32_t k_voff = (uint32_t)k_key_l * KROW + k_chunk_l;
+    const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
+    auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
         const int t0 = j * BC;
-        for (int c0 = t_first * 64; c0 < K_CH; c0 += t_count * 64) {
-            const int c = c0 + lane;
-            const int r = c / KCHR;
-            int ch = c - r * KCHR;
-            ch = ch == KCHR - 1 ? 0 : ch;
-            const int key = min(t0 + 32 * (r >> 5) + a_row_to_key(r & 31), N - 1);
-            g2lds16(Kg + (size_t)key * KROW + ch * 16, dst + c0 * 16);
+        if (t0 + BC <= N) {
+#pragma unroll
+            for (int it = 0; it < K_NI; ++it)
+                g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
+                        dst + (wl + 4 * it) * 1024);
+        } else {
+#pragma unroll
+            for (int it = 0; it < K_NI; ++it) {
+                const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, N - 1);
+                g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
+            }
         }
     };
-    auto load_v = [&](uint8_t* dst, int j, int t_first, int t_count) __attribute__((always_inline)) {
+    auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
         const int t0 = j * BC;
-        for (int c0 = t_first * 64; c0 < V_CH; c0 += t_count * 64) {
-            const int c = c0 + lane;
-            const int r = c / VCHR;
-            int ch = c - r * VCHR;
-            ch = ch == VCHR - 1 ? 0 : ch;
-            const int key = min(t0 + r, N - 1);
-            g2lds16(Vg + (size_t)key * D + ch * 16, dst + c0 * 16);
+        if (t0 + BC <= N) {
+#pragma unroll
+            for (int it = 0; it < V_NI; ++it)
+                g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
+        } else {
+#pragma unroll
+            for (int it = 0; it < V_NI; ++it) {
+                const int key = min(t0 + 4 * V_RPI * it + v_key_l, N - 1);
+                g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
+            }
         }
     };
 
@@ -159,10 +200,16 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                 qf[kk][i] = (__bf16)0.f;
     }
 
-    // per-lane LDS offsets; every fragment read is base + an immediate
-    const int k_lane = n * KS + 16 * h;                       // S^T A operand: LDS row n, chunk 2kk + h
+    // per-lane LDS offsets.  S^T A operand of k-step kk, tile kt: LDS row
+    // 32 kt + n, logical chunk 2 kk + h, i.e. (k_lane ^ (kk << 5)) + kt 32 KROW.
+    // V^T operand of d-tile dt: rows (j16 >> 1) + 16 h + {0, 8, 32, 40} + 64 js,
+    // logical chunk 2 dt + (n >> 4), half j16 & 1, i.e. (v_lane ^ (dt << 5)) +
+    // row offset.  (The XOR only touches chunk bits; row offsets are
+    // multiples of 8 rows and leave both swizzles unchanged.)
+    const uint32_t k_lane = (uint32_t)(n * KROW + ((h ^ kswz(n)) << 4));
     const int j16 = n & 15;                                   // lane within its 16-lane group
-    const int v_lane = ((j16 >> 1) + 16 * h) * VS + 16 * (n >> 4) + 8 * (j16 & 1);
+    const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
+                                       8 * (j16 & 1));
 
     const float c = p.c;
     const float S = p.S;
@@ -186,16 +233,18 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     // matrix core instead of stalling every MFMA; sched_barrier keeps the
     // compiler from sinking the reads back next to their uses.
     auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
-        const uint8_t* kb = kst + k_lane;
+        auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
+            return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
+        };
         bf16x8 a0[KT], a1[KT];
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt)
-            a0[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS);
+            a0[kt] = kfrag(0, kt);
 #pragma unroll
         for (int kk = 0; kk < DK; kk += 2) {
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
-                a1[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS + (kk + 1) * 32);
+                a1[kt] = kfrag(kk + 1, kt);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
@@ -208,7 +257,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             if (kk + 2 < DK) {
 #pragma unroll
                 for (int kt = 0; kt < KT; ++kt)
-                    a0[kt] = *reinterpret_cast<const bf16x8*>(kb + kt * 32 * KS + (kk + 2) * 32);
+                    a0[kt] = kfrag(kk + 2, kt);
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -222,13 +271,12 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     // V^T operands of the next MFMA are read (transposed) while the current
     // one runs.
     auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
-        const uint8_t* vb = vst + v_lane;
         auto vload = [&](int js, int dt) __attribute__((always_inline)) {
-            const uint8_t* va = vb + 32 * dt + 64 * js * VS;
+            const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
             const i32x2 r0 = lds_read_tr8(va);
-            const i32x2 r1 = lds_read_tr8(va + 8 * VS);
-            const i32x2 r2 = lds_read_tr8(va + 32 * VS);
-            const i32x2 r3 = lds_read_tr8(va + 40 * VS);
+            const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
+            const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
+            const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
             return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
         };
         i32x8 anext = vload(0, 0);
@@ -380,8 +428,9 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         mc_run = mc_new;
     };
 
-    // ---- prologue: K of the first block into stage 0 (all waves) ----
-    load_k(Ks0, jof(0), w, NW);
+    // ---- prologue: K of the first block into stage 0 ----
+    if (grp == 0)
+        load_k(Ks0, jof(0));
     // Q fragments and the first K stage are complete after this point; the
     // compiler sees the wait (it tracks no outstanding loads in the loop)
     __builtin_amdgcn_s_waitcnt(0);
@@ -400,9 +449,9 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         __attribute__((always_inline)) {
         if (grp == 0) {
             if (k + 1 < nb)
-                load_k(k_nxt, jof(k + 1), w, 4);
+                load_k(k_nxt, jof(k + 1));
             if (k < nb)
-                load_v(v_cur, jof(k), w, 4);
+                load_v(v_cur, jof(k));
         }
         if (valid(k - 1))
             pv(v_prv);
