@@ -224,54 +224,50 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         for (int r = 0; r < 16; ++r)
             o[dt][r] = 0.f;
     f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
-    uint32_t pk[KT][4];           // E4M3 P bytes between the VALU and the next MFMA phase
+    uint32_t pk[KT][4] = {};      // E4M3 P bytes between the VALU and the next MFMA phase
     uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
 
     // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
-    // The K fragments of k-step kk+1 are requested before the four MFMAs of
-    // step kk are issued (two register sets), so the LDS latency overlaps the
-    // matrix core instead of stalling every MFMA; sched_barrier keeps the
-    // compiler from sinking the reads back next to their uses.
+    // The K fragments of k-step kk+2 are requested before the MFMAs of step
+    // kk are issued (three rotating register sets), so LDS latency and the
+    // CU-wide LDS bandwidth (shared with three other waves in this phase)
+    // overlap the matrix core; sched_barrier keeps the compiler from sinking
+    // the reads back next to their uses.
     auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
         auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
             return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
         };
-        bf16x8 a0[KT], a1[KT];
+        constexpr int PF = DK >= 3 ? 2 : DK - 1;    // prefetch distance in k-steps
+        bf16x8 a[PF + 1][KT];
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-            a0[kt] = kfrag(0, kt);
-#pragma unroll
-        for (int kk = 0; kk < DK; kk += 2) {
+        for (int kk = 0; kk < PF; ++kk)
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
-                a1[kt] = kfrag(kk + 1, kt);
+                a[kk][kt] = kfrag(kk, kt);
+#pragma unroll
+        for (int kk = 0; kk < DK; ++kk) {
+            if (kk + PF < DK) {
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+                    a[(kk + PF) % (PF + 1)][kt] = kfrag(kk + PF, kt);
+            }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
                 if (kk == 0)
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kt], qf[kk], f32x16{}, 0, 0, 0);
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kt], qf[0], f32x16{}, 0, 0, 0);
                 else
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[kt], qf[kk], s[kt], 0, 0, 0);
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk % (PF + 1)][kt], qf[kk], s[kt], 0, 0, 0);
             }
-            __builtin_amdgcn_sched_barrier(0);
-            if (kk + 2 < DK) {
-#pragma unroll
-                for (int kt = 0; kt < KT; ++kt)
-                    a0[kt] = kfrag(kk + 2, kt);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int kt = 0; kt < KT; ++kt)
-                s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[kt], qf[kk + 1], s[kt], 0, 0, 0);
             __builtin_amdgcn_sched_barrier(0);
         }
     };
 
     // ---- O^T += V_j^T P8^T ----
-    // V^T operands of the next MFMA are read (transposed) while the current
-    // one runs.
+    // The V^T operands are read (transposed) two MFMAs ahead of their use.
     auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
-        auto vload = [&](int js, int dt) __attribute__((always_inline)) {
+        auto vload = [&](int i) __attribute__((always_inline)) {
+            const int js = i / DT, dt = i % DT;
             const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
             const i32x2 r0 = lds_read_tr8(va);
             const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
@@ -279,26 +275,26 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
             return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
         };
-        i32x8 anext = vload(0, 0);
+        constexpr int NM = PVS * DT;                 // FP8 MFMAs per block
+        constexpr int PF = NM >= 3 ? 2 : NM - 1;
+        i32x8 av[PF + 1];
 #pragma unroll
-        for (int js = 0; js < PVS; ++js) {
+        for (int i = 0; i < PF; ++i)
+            av[i] = vload(i);
+#pragma unroll
+        for (int i = 0; i < NM; ++i) {
+            const int js = i / DT, dt = i % DT;
+            if (i + PF < NM)
+                av[(i + PF) % (PF + 1)] = vload(i + PF);
             i32x8 bop;
 #pragma unroll
             for (int q4 = 0; q4 < 4; ++q4) {
                 bop[q4] = (int)pk[2 * js][q4];
                 bop[4 + q4] = (int)pk[2 * js + 1][q4];
             }
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt) {
-                const i32x8 aop = anext;
-                if (dt + 1 < DT)
-                    anext = vload(js, dt + 1);
-                else if (js + 1 < PVS)
-                    anext = vload(js + 1, 0);
-                __builtin_amdgcn_sched_barrier(0);
-                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(aop, bop, o[dt], 0, 0, 0, 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(0);
-            }
+            __builtin_amdgcn_sched_barrier(0);
+            o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0, 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
     };
 
@@ -388,18 +384,20 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                 const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
                 const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
                 uint32_t word;
+                // The first convert writes the low half of the word, the second
+                // the high half; the stale bytes of the previous block that the
+                // word starts from are all overwritten (no zeroing needed).
                 if constexpr (POW2) {
-                    // (the first convert writes the low half, the second the high half)
-                    s16x2 lo = {0, 0};
+                    s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
                     lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, inv_S, false);
                     lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, inv_S, true);
-                    word = ((uint32_t)(uint16_t)lo[1] << 16) | (uint32_t)(uint16_t)lo[0];
+                    word = __builtin_bit_cast(uint32_t, lo);
                 } else {
                     const float y0 = __builtin_fminf(p0 * S, 448.f);
                     const float y1 = __builtin_fminf(p1 * S, 448.f);
                     const float y2 = __builtin_fminf(p2 * S, 448.f);
                     const float y3 = __builtin_fminf(p3 * S, 448.f);
-                    int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false);
+                    int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)pk[kt][r4], false);
                     wv = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, wv, true);
                     word = (uint32_t)wv;
                 }
