@@ -22,6 +22,7 @@ _LIB_PATH = os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 ORDER = {"forward": 0, "reverse": 1}
+SCALE = {"static": 0, "dynamic": 1}
 
 
 def build(force: bool = True) -> str:
@@ -51,7 +52,7 @@ def lib() -> ctypes.CDLL:
         L.oracle_e4m3_encode_array.restype = None
         L.oracle_e4m3_decode_array.argtypes = [P, P, i64]
         L.oracle_e4m3_decode_array.restype = None
-        L.oracle_attn.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, P, i64, i32]
+        L.oracle_attn.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, i32, P, i64, i32]
         L.oracle_attn.restype = i32
         L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
         L.oracle_ref_fp64.restype = i32
@@ -89,11 +90,14 @@ def e4m3_decode(codes) -> np.ndarray:
 
 
 def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
-         cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None):
+         cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None,
+         scale: str = "static"):
     """Algorithm 1 on the given rows.
 
     q: [B,Hq,N,d]; k, v: [B,Hkv,N,d]; float32 arrays holding the exact values
     the device consumed.  rows: flat row ids ((b*Hq+hq)*N + r) or None for all.
+    scale: "static" (one S for every block) or "dynamic" (per-block 2^kj from
+    the block's P range, S = 2^k0 its floor; see oracle.c).
     Returns (out [n_rows,d] float32, lse [n_rows] float32, counts [n_rows,3] uint32).
     """
     q = np.ascontiguousarray(q, dtype=np.float32)
@@ -112,7 +116,7 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     counts = np.zeros((n_rows, 3), dtype=np.uint32)
     rc = lib().oracle_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
                            B, Hq, Hkv, N, d, int(bool(causal)), int(block_kv),
-                           ORDER[order], float(S), int(bool(cast)), int(n_sink),
+                           ORDER[order], float(S), int(bool(cast)), SCALE[scale], int(n_sink),
                            _ptr(rows_a), n_rows, nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_attn rejected its arguments")

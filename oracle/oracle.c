@@ -19,6 +19,9 @@
  *     O / (S * l).
  *   - Prop. 1 (P-underflow condition): a P value underflows when its code is
  *     zero; the diagnostic counts those codes per key category.
+ *   - Limitations and Future Work, "worst-case vs average-case": a dynamic
+ *     per-block power-of-two scale, chosen from the block's P range (only
+ *     sketched in the paper; the rule below is this oracle's reading).
  *
  * Readings where the paper leaves the arithmetic open (each also listed in
  * the design notes of the repository):
@@ -32,6 +35,13 @@
  *     last block first; under causal masking a row visits only the blocks
  *     holding at least one key t <= r, and masked keys take no part in l, O or
  *     the counts.
+ *   - dynamic scale (scale_mode 1, S = 2^k0 with 0 <= k0 <= 8): block j of a
+ *     row casts with S_j = 2^kj, kj = min(k0 + max(0, floor(-xmax)), 126),
+ *     xmax = fma(max_t D_t, c, -mc) the block's largest exponent argument, so
+ *     the block's largest P lands in (S/2, S] as the static scale puts P = 1;
+ *     a block that holds the running maximum keeps kj = k0.  The decoded value
+ *     is taken back to S units exactly (times 2^(k0 - kj)), so O, l and the
+ *     epilogue are those of the static scale.
  */
 #include <math.h>
 #include <pthread.h>
@@ -39,7 +49,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORACLE_VERSION 1
+#define ORACLE_VERSION 2
 
 /* ------------------------------------------------------------------------- */
 /* OCP E4M3 (Sec. 2.1)                                                        */
@@ -126,6 +136,7 @@ void oracle_e4m3_decode_array(const uint8_t* x, float* out, int64_t n)
 
 enum { ORDER_FORWARD = 0, ORDER_REVERSE = 1 };
 enum { CAST_NONE = 0, CAST_E4M3 = 1 };
+enum { SCALE_STATIC = 0, SCALE_DYNAMIC = 1 };
 
 typedef struct {
     const float* q;     /* [B][Hq][N][d]  */
@@ -135,6 +146,7 @@ typedef struct {
     float* lse;         /* [n_rows]       (nullable) */
     uint32_t* counts;   /* [n_rows][3]    (nullable) */
     int B, Hq, Hkv, N, d, causal, Bc, order, cast, n_sink;
+    int scale_mode, k0;     /* k0 = log2 S (dynamic scale only) */
     float S;
     const int64_t* rows;/* flat (b*Hq + hq)*N + r, n_rows of them */
     int64_t n_rows;
@@ -201,10 +213,24 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         }
         ell = alpha * ell + psum;
 
-        /* P-cast: P_fp8 = cast_E4M3(P * S); the P-underflow diagnostic counts
-         * zero codes per key category */
+        /* scale of this block's cast: S, or with the dynamic scale 2^kj
+         * chosen from the block's largest exponent argument */
+        float Sj = S;
+        int back = 0;                           /* S units = block units * 2^back */
+        if (J->scale_mode == SCALE_DYNAMIC) {
+            const float xmax = fmaf(mloc, c, -mc_new);
+            const double f = floor(-(double)xmax);
+            int kj = J->k0 + (f > 0.0 ? (f > 200.0 ? 200 : (int)f) : 0);
+            if (kj > 126)
+                kj = 126;
+            Sj = ldexpf(1.0f, kj);
+            back = J->k0 - kj;
+        }
+
+        /* P-cast: P_fp8 = cast_E4M3(P * Sj); the P-underflow diagnostic counts
+         * zero codes per key category; the decoded value goes back to S units */
         for (int t = 0; t < nt; t++) {
-            const float y = P[t] * S;
+            const float y = P[t] * Sj;
             if (J->cast == CAST_E4M3) {
                 const uint8_t e = oracle_e4m3_encode(y);
                 if (cnt_row && e == 0x00) {
@@ -212,9 +238,9 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
                     const int cat = key < J->n_sink ? 0 : (key < Bc ? 1 : 2);
                     cnt_row[cat]++;
                 }
-                P[t] = oracle_e4m3_decode(e);
+                P[t] = ldexpf(oracle_e4m3_decode(e), back);
             } else {
-                P[t] = y;
+                P[t] = ldexpf(y, back);
             }
         }
 
@@ -298,18 +324,29 @@ static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
  *   out: [n_rows][d], lse: [n_rows] (nullable), counts: [n_rows][3]
  *   (nullable; categories key < n_sink, n_sink <= key < Bc, key >= Bc).
  *   cast: 0 = no cast (P*S used as is), 1 = E4M3.
+ *   scale_mode: 0 = static S, 1 = dynamic per-block 2^kj (S must be 2^k0,
+ *   0 <= k0 <= 8).
  * Returns 0, or -1 on an invalid argument.
  */
 int oracle_attn(const float* q, const float* k, const float* v, float* out,
                 float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
                 int d, int causal, int block_kv, int order, float S, int cast,
-                int n_sink, const int64_t* rows, int64_t n_rows, int nthreads)
+                int scale_mode, int n_sink, const int64_t* rows, int64_t n_rows,
+                int nthreads)
 {
     if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
         d < 1 || Hq % Hkv != 0 || block_kv < 1 || !(S > 0.0f) ||
         !isfinite(S) || (order != 0 && order != 1) || (cast != 0 && cast != 1) ||
-        n_sink < 0 || n_rows < 0)
+        (scale_mode != 0 && scale_mode != 1) || n_sink < 0 || n_rows < 0)
         return -1;
+    int k0 = 0;
+    if (scale_mode == SCALE_DYNAMIC) {
+        int e;
+        const float f = frexpf(S, &e);          /* S = f * 2^e, f in [0.5, 1) */
+        k0 = e - 1;
+        if (f != 0.5f || k0 < 0 || k0 > 8)
+            return -1;
+    }
     if (rows)
         for (int64_t i = 0; i < n_rows; i++)
             if (rows[i] < 0 || rows[i] >= (int64_t)B * Hq * N)
@@ -321,6 +358,7 @@ int oracle_attn(const float* q, const float* k, const float* v, float* out,
     J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse; J.counts = counts;
     J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
     J.Bc = block_kv; J.order = order; J.cast = cast; J.n_sink = n_sink;
+    J.scale_mode = scale_mode; J.k0 = k0;
     J.S = S; J.rows = rows; J.n_rows = n_rows; J.nthreads = nthreads;
     run_threads(attn_worker, &J, &J.lock, nthreads);
     return 0;
