@@ -43,6 +43,10 @@ struct Params {
     int n_tiles;         // query tiles per (batch, head)
     int total_wg;        // B * Hq * n_tiles
     int per_xcd;         // ceil(total_wg / 8)
+    // persistent schedule (fast kernel): a work unit is a pair of query
+    // tiles (t, n_tiles - 1 - t) of one (batch, head)
+    int pairs;           // units per (batch, head) = ceil(n_tiles / 2)
+    long long units;     // B * Hq * pairs
 };
 
 constexpr int kNumXcd = 8;   // MI355X: 8 XCDs x 32 CUs, workgroup i runs on XCD i % 8
@@ -67,6 +71,32 @@ __device__ inline bool map_tile(const Params& p, int& bh, int& tile)
     const int t = L - bh * p.n_tiles;
     tile = CAUSAL ? (p.n_tiles - 1 - t) : t;
     return true;
+}
+
+// Persistent schedule of the fast kernel.  The grid holds one workgroup per
+// CU (8 XCDs x gridDim.x / 8 CUs).  Work units -- pairs of query tiles
+// (t, T - 1 - t) of one (batch, head) -- are numbered head-major and split
+// into 8 contiguous ranges, one per XCD, so the heads of an XCD (and the
+// query heads of a GQA group) stream their K/V through one L2.  Inside its
+// range a workgroup takes every (gridDim.x / 8)-th unit.  Under causal
+// masking a tile pair costs the same for every t (the blocks of tile t plus
+// those of tile T - 1 - t), so every CU gets the same amount of work; the
+// heavier tile of a pair runs first.
+struct UnitRange {
+    long long begin, end;   // this XCD's units
+    int first, stride;      // first unit offset and stride of this workgroup
+};
+
+__device__ inline UnitRange unit_range(const Params& p)
+{
+    const int xcd = blockIdx.x % kNumXcd;
+    const int per = gridDim.x / kNumXcd;
+    UnitRange r;
+    r.begin = p.units * xcd / kNumXcd;
+    r.end = p.units * (xcd + 1) / kNumXcd;
+    r.first = blockIdx.x / kNumXcd;
+    r.stride = per;
+    return r;
 }
 
 // Key permutation inside a 32-key S^T tile: MFMA A-row m -> key offset, so that

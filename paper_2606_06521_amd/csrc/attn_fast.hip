@@ -17,6 +17,10 @@
 // barrier between phases.  On every SIMD one wave keeps the matrix core busy
 // while the other runs the softmax.
 //
+// Grid: persistent, one workgroup per CU; each takes tile pairs (t, T-1-t)
+// of the heads of its XCD (unit_range), which equalises the causal work per
+// CU.
+//
 // K_j and V_j go global -> LDS with no register staging
 // (global_load_lds_dwordx4, lane i -> LDS base + 16 i), double-buffered, issued
 // by group 0 at the start of its MFMA phase two phases before first use.
@@ -103,439 +107,455 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     // LDS row of a K stage -> key offset in the block
     auto krow_key = [](int r) __attribute__((always_inline)) { return 32 * (r >> 5) + a_row_to_key(r & 31); };
 
-    int bh, tile;
-    if (!map_tile<CAUSAL>(p, bh, tile))
-        return;
-    const int N = p.N;
-    const int b = bh / p.Hq;
-    const int hq = bh - b * p.Hq;
-    const int hk = hq / (p.Hq / p.Hkv);
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, scalar
-    const int grp = w >> 2;                                   // 0: waves 0-3, 1: waves 4-7
-    const int n = lane & 31;
-    const int h = lane >> 5;
-    const int row0 = tile * BM;
-    const int wrow0 = row0 + 32 * w;
-    const int row = wrow0 + n;
+    // ---- persistent loop over this workgroup's tile pairs (heavier tile first) ----
+    const UnitRange ur = unit_range(p);
+    const int T = p.n_tiles;
+    for (long long u = ur.begin + ur.first; u < ur.end; u += ur.stride) {
+    for (int half = 0; half < 2; ++half) {
+        const int bh = (int)(u / p.pairs);
+        const int pr = (int)(u - (long long)bh * p.pairs);
+        const int tile = half == 0 ? T - 1 - pr : pr;
+        if (half == 1 && tile == T - 1 - pr)
+            break;                                    // odd tile count: the middle tile is alone
+        const int N = p.N;
+        const int b = bh / p.Hq;
+        const int hq = bh - b * p.Hq;
+        const int hk = hq / (p.Hq / p.Hkv);
+        const int tid = threadIdx.x;
+        const int lane = tid & 63;
+        const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, scalar
+        const int grp = w >> 2;                                   // 0: waves 0-3, 1: waves 4-7
+        const int n = lane & 31;
+        const int h = lane >> 5;
+        const int row0 = tile * BM;
+        const int wrow0 = row0 + 32 * w;
+        const int row = wrow0 + n;
 
-    const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * N * KROW;
-    const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)N;
-    const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
-    const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * D;
+        const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * N * KROW;
+        const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)N;
+        const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
+        const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * D;
 
-    const int last_row_wg = min(row0 + BM, N) - 1;
-    const int nb = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
-    const bool wave_on = wrow0 < N;
-    // every row of a wave lies in one BC-block of rows (BC is a multiple of 32)
-    const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nb;
-    auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
-    auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
+        const int last_row_wg = min(row0 + BM, N) - 1;
+        const int nb = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
+        const bool wave_on = wrow0 < N;
+        // every row of a wave lies in one BC-block of rows (BC is a multiple of 32)
+        const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nb;
+        auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
+        auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
 
-    // ---- direct global -> LDS loads of one K / V stage (waves 0-3) ----
-    // Load instruction i = wl + 4 it of a stage (wl = w & 3) writes LDS bytes
-    // [1024 i, +1024): lane l fills row 4 K_RPI it + rho, rho = wl K_RPI +
-    // l / KCPR, physical chunk l % KCPR, i.e. logical chunk
-    // (l % KCPR) ^ kswz(rho) of key krow_key(4 K_RPI it) + krow_key(rho)
-    // (4 K_RPI is a power of two >= 16, so the two key parts have disjoint
-    // bits and the swizzle does not depend on it).  V likewise with
-    // key = row.  Keys past the end of the sequence (only in a ragged last
-    // block) read row N-1: they are masked to P = 0 before they can contribute.
-    const int wl = w & 3;
-    int k_key_l, v_key_l;
-    uint32_t k_chunk_l, v_chunk_l;
-    {
-        const int rk = wl * K_RPI + lane / KCPR;
-        k_key_l = krow_key(rk);
-        k_chunk_l = (uint32_t)(((lane % KCPR) ^ kswz(rk)) * 16);
-        const int rv = wl * V_RPI + lane / VCPR;
-        v_key_l = rv;
-        v_chunk_l = (uint32_t)(((lane % VCPR) ^ vswz(rv)) * 16);
-    }
-    const uint32_t k_voff = (uint32_t)k_key_l * KROW + k_chunk_l;
-    const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
-    auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
-        const int t0 = j * BC;
-        if (t0 + BC <= N) {
-#pragma unroll
-            for (int it = 0; it < K_NI; ++it)
-                g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
-                        dst + (wl + 4 * it) * 1024);
-        } else {
-#pragma unroll
-            for (int it = 0; it < K_NI; ++it) {
-                const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, N - 1);
-                g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
-            }
+        // ---- direct global -> LDS loads of one K / V stage (waves 0-3) ----
+        // Load instruction i = wl + 4 it of a stage (wl = w & 3) writes LDS bytes
+        // [1024 i, +1024): lane l fills row 4 K_RPI it + rho, rho = wl K_RPI +
+        // l / KCPR, physical chunk l % KCPR, i.e. logical chunk
+        // (l % KCPR) ^ kswz(rho) of key krow_key(4 K_RPI it) + krow_key(rho)
+        // (4 K_RPI is a power of two >= 16, so the two key parts have disjoint
+        // bits and the swizzle does not depend on it).  V likewise with
+        // key = row.  Keys past the end of the sequence (only in a ragged last
+        // block) read row N-1: they are masked to P = 0 before they can contribute.
+        const int wl = w & 3;
+        int k_key_l, v_key_l;
+        uint32_t k_chunk_l, v_chunk_l;
+        {
+            const int rk = wl * K_RPI + lane / KCPR;
+            k_key_l = krow_key(rk);
+            k_chunk_l = (uint32_t)(((lane % KCPR) ^ kswz(rk)) * 16);
+            const int rv = wl * V_RPI + lane / VCPR;
+            v_key_l = rv;
+            v_chunk_l = (uint32_t)(((lane % VCPR) ^ vswz(rv)) * 16);
         }
-    };
-    auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
-        const int t0 = j * BC;
-        if (t0 + BC <= N) {
+        const uint32_t k_voff = (uint32_t)k_key_l * KROW + k_chunk_l;
+        const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
+        auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if (t0 + BC <= N) {
 #pragma unroll
-            for (int it = 0; it < V_NI; ++it)
-                g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
-        } else {
+                for (int it = 0; it < K_NI; ++it)
+                    g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
+                            dst + (wl + 4 * it) * 1024);
+            } else {
 #pragma unroll
-            for (int it = 0; it < V_NI; ++it) {
-                const int key = min(t0 + 4 * V_RPI * it + v_key_l, N - 1);
-                g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
-            }
-        }
-    };
-
-    // Q^T fragments (B operand): lane (n, h) holds Q[row][16*kk + 8*h .. +8]
-    bf16x8 qf[DK];
-    if (row < N) {
-        const uint8_t* qr = Qg + (size_t)row * KROW;
-#pragma unroll
-        for (int kk = 0; kk < DK; ++kk)
-            qf[kk] = *reinterpret_cast<const bf16x8*>(qr + (16 * kk + 8 * h) * 2);
-    } else {
-#pragma unroll
-        for (int kk = 0; kk < DK; ++kk)
-#pragma unroll
-            for (int i = 0; i < 8; ++i)
-                qf[kk][i] = (__bf16)0.f;
-    }
-
-    // per-lane LDS offsets.  S^T A operand of k-step kk, tile kt: LDS row
-    // 32 kt + n, logical chunk 2 kk + h, i.e. (k_lane ^ (kk << 5)) + kt 32 KROW.
-    // V^T operand of d-tile dt: rows (j16 >> 1) + 16 h + {0, 8, 32, 40} + 64 js,
-    // logical chunk 2 dt + (n >> 4), half j16 & 1, i.e. (v_lane ^ (dt << 5)) +
-    // row offset.  (The XOR only touches chunk bits; row offsets are
-    // multiples of 8 rows and leave both swizzles unchanged.)
-    const uint32_t k_lane = (uint32_t)(n * KROW + ((h ^ kswz(n)) << 4));
-    const int j16 = n & 15;                                   // lane within its 16-lane group
-    const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
-                                       8 * (j16 & 1));
-
-    const float c = p.c;
-    const float S = p.S;
-    const float inv_S = p.inv_S;
-    float m_run = -INFINITY;
-    float mc_run = -INFINITY;
-    float ell = 0.f;
-    f32x16 o[DT];
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r)
-            o[dt][r] = 0.f;
-    f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
-    uint32_t pk[KT][4] = {};      // E4M3 P bytes between the VALU and the next MFMA phase
-    uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
-
-    // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
-    // The K fragments of k-step kk+2 are requested before the MFMAs of step
-    // kk are issued (three rotating register sets), so LDS latency and the
-    // CU-wide LDS bandwidth (shared with three other waves in this phase)
-    // overlap the matrix core; sched_barrier keeps the compiler from sinking
-    // the reads back next to their uses.
-    auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
-        auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
-            return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
-        };
-        constexpr int PF = DK >= 3 ? 2 : DK - 1;    // prefetch distance in k-steps
-        bf16x8 a[PF + 1][KT];
-#pragma unroll
-        for (int kk = 0; kk < PF; ++kk)
-#pragma unroll
-            for (int kt = 0; kt < KT; ++kt)
-                a[kk][kt] = kfrag(kk, kt);
-#pragma unroll
-        for (int kk = 0; kk < DK; ++kk) {
-            if (kk + PF < DK) {
-#pragma unroll
-                for (int kt = 0; kt < KT; ++kt)
-                    a[(kk + PF) % (PF + 1)][kt] = kfrag(kk + PF, kt);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int kt = 0; kt < KT; ++kt) {
-                if (kk == 0)
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kt], qf[0], f32x16{}, 0, 0, 0);
-                else
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk % (PF + 1)][kt], qf[kk], s[kt], 0, 0, 0);
-            }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-
-    // ---- O^T += V_j^T P8^T ----
-    // The V^T operands are read (transposed) two MFMAs ahead of their use.
-    auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
-        auto vload = [&](int i) __attribute__((always_inline)) {
-            const int js = i / DT, dt = i % DT;
-            const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
-            const i32x2 r0 = lds_read_tr8(va);
-            const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
-            const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
-            const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
-            return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
-        };
-        constexpr int NM = PVS * DT;                 // FP8 MFMAs per block
-        constexpr int PF = NM >= 3 ? 2 : NM - 1;
-        i32x8 av[PF + 1];
-#pragma unroll
-        for (int i = 0; i < PF; ++i)
-            av[i] = vload(i);
-#pragma unroll
-        for (int i = 0; i < NM; ++i) {
-            const int js = i / DT, dt = i % DT;
-            if (i + PF < NM)
-                av[(i + PF) % (PF + 1)] = vload(i + PF);
-            i32x8 bop;
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-                bop[q4] = (int)pk[2 * js][q4];
-                bop[4 + q4] = (int)pk[2 * js + 1][q4];
-            }
-            __builtin_amdgcn_sched_barrier(0);
-            o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0, 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
-        }
-    };
-
-    // ---- running max, alpha, P, l (pre-cast), E4M3 cast, rescale of O ----
-    auto softmax = [&](int j) __attribute__((always_inline)) {
-        const int t0 = j * BC;
-        if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
-            // key t0 + 32 kt + 16 h + r is valid iff 32 kt + r <= lim; masked
-            // scores become -inf through a sign-mask bit select (no compares)
-            const int lim = (CAUSAL ? min(row, N - 1) : N - 1) - t0 - 16 * h;
-#pragma unroll
-            for (int kt = 0; kt < KT; ++kt)
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const uint32_t m = (uint32_t)((lim - (32 * kt + r)) >> 31);
-                    const float sv = s[kt][r];
-                    const uint32_t x = __float_as_uint(sv);
-                    s[kt][r] = __uint_as_float((x & ~m) | (0xFF800000u & m));
+                for (int it = 0; it < K_NI; ++it) {
+                    const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, N - 1);
+                    g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
                 }
+            }
+        };
+        auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if (t0 + BC <= N) {
+#pragma unroll
+                for (int it = 0; it < V_NI; ++it)
+                    g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
+            } else {
+#pragma unroll
+                for (int it = 0; it < V_NI; ++it) {
+                    const int key = min(t0 + 4 * V_RPI * it + v_key_l, N - 1);
+                    g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
+                }
+            }
+        };
+
+        // Q^T fragments (B operand): lane (n, h) holds Q[row][16*kk + 8*h .. +8]
+        bf16x8 qf[DK];
+        if (row < N) {
+            const uint8_t* qr = Qg + (size_t)row * KROW;
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk)
+                qf[kk] = *reinterpret_cast<const bf16x8*>(qr + (16 * kk + 8 * h) * 2);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk)
+#pragma unroll
+                for (int i = 0; i < 8; ++i)
+                    qf[kk][i] = (__bf16)0.f;
         }
-        // row maximum: one independent chain per 32-key tile, then the tiles,
-        // then the two lane halves (a maximum is exact in any order)
-        float mk[KT];
+
+        // per-lane LDS offsets.  S^T A operand of k-step kk, tile kt: LDS row
+        // 32 kt + n, logical chunk 2 kk + h, i.e. (k_lane ^ (kk << 5)) + kt 32 KROW.
+        // V^T operand of d-tile dt: rows (j16 >> 1) + 16 h + {0, 8, 32, 40} + 64 js,
+        // logical chunk 2 dt + (n >> 4), half j16 & 1, i.e. (v_lane ^ (dt << 5)) +
+        // row offset.  (The XOR only touches chunk bits; row offsets are
+        // multiples of 8 rows and leave both swizzles unchanged.)
+        const uint32_t k_lane = (uint32_t)(n * KROW + ((h ^ kswz(n)) << 4));
+        const int j16 = n & 15;                                   // lane within its 16-lane group
+        const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
+                                           8 * (j16 & 1));
+
+        const float c = p.c;
+        const float S = p.S;
+        const float inv_S = p.inv_S;
+        float m_run = -INFINITY;
+        float mc_run = -INFINITY;
+        float ell = 0.f;
+        f32x16 o[DT];
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) {
-            float a = s[kt][0];
-#pragma unroll
-            for (int r = 1; r < 16; ++r)
-                a = fmax_f(a, s[kt][r]);
-            mk[kt] = a;
-        }
-        float mx = mk[0];
-#pragma unroll
-        for (int kt = 1; kt < KT; ++kt)
-            mx = fmax_f(mx, mk[kt]);
-        mx = halves_max(mx);
-        const float m_new = fmax_f(m_run, mx);
-        const float mc_new = m_new * c;
-        const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
-        const float nmc = -mc_new;
-        // The rest is organised in stages so that no instruction waits on the
-        // result of the one just before it (this phase runs alone on its
-        // SIMD's vector ALU while the partner wave drives the matrix core):
-        // (1) x = fma(D, c, -mc) for all keys, in place;
-        // (2) P = exp2(x) for all keys, in place, interleaved with the rescale
-        //     of O (independent work for the vector ALU while exp2 is in flight);
-        // (3) l from the pre-cast P (one partial sum per tile), E4M3 cast.
-#pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
             for (int r = 0; r < 16; ++r)
-                s[kt][r] = __builtin_fmaf(s[kt][r], c, nmc);
-        __builtin_amdgcn_sched_barrier(0);
-        // rescale O before this block's P.V; skipped when no row of the wave
-        // moved its maximum (alpha is then exactly 1)
-        const bool rescale = __ballot(alpha != 1.0f) != 0;
-        if (rescale) {
+                o[dt][r] = 0.f;
+        f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
+        uint32_t pk[KT][4] = {};      // E4M3 P bytes between the VALU and the next MFMA phase
+        uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
+
+        // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
+        // The K fragments of k-step kk+2 are requested before the MFMAs of step
+        // kk are issued (three rotating register sets), so LDS latency and the
+        // CU-wide LDS bandwidth (shared with three other waves in this phase)
+        // overlap the matrix core; sched_barrier keeps the compiler from sinking
+        // the reads back next to their uses.
+        auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
+            auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
+                return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
+            };
+            constexpr int PF = DK >= 3 ? 2 : DK - 1;    // prefetch distance in k-steps
+            bf16x8 a[PF + 1][KT];
 #pragma unroll
-            for (int t = 0; t < DT; ++t)
+            for (int kk = 0; kk < PF; ++kk)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    o[t][r] *= alpha;
-        }
-        {
+                for (int kt = 0; kt < KT; ++kt)
+                    a[kk][kt] = kfrag(kk, kt);
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk) {
+                if (kk + PF < DK) {
+#pragma unroll
+                    for (int kt = 0; kt < KT; ++kt)
+                        a[(kk + PF) % (PF + 1)][kt] = kfrag(kk + PF, kt);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt) {
+                    if (kk == 0)
+                        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0][kt], qf[0], f32x16{}, 0, 0, 0);
+                    else
+                        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk % (PF + 1)][kt], qf[kk], s[kt], 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // ---- O^T += V_j^T P8^T ----
+        // The V^T operands are read (transposed) two MFMAs ahead of their use.
+        auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
+            auto vload = [&](int i) __attribute__((always_inline)) {
+                const int js = i / DT, dt = i % DT;
+                const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
+                const i32x2 r0 = lds_read_tr8(va);
+                const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
+                const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
+                const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
+                return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+            };
+            constexpr int NM = PVS * DT;                 // FP8 MFMAs per block
+            constexpr int PF = NM >= 3 ? 2 : NM - 1;
+            i32x8 av[PF + 1];
+#pragma unroll
+            for (int i = 0; i < PF; ++i)
+                av[i] = vload(i);
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                const int js = i / DT, dt = i % DT;
+                if (i + PF < NM)
+                    av[(i + PF) % (PF + 1)] = vload(i + PF);
+                i32x8 bop;
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    bop[q4] = (int)pk[2 * js][q4];
+                    bop[4 + q4] = (int)pk[2 * js + 1][q4];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0, 0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // ---- running max, alpha, P, l (pre-cast), E4M3 cast, rescale of O ----
+        auto softmax = [&](int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
+                // key t0 + 32 kt + 16 h + r is valid iff 32 kt + r <= lim; masked
+                // scores become -inf through a sign-mask bit select (no compares)
+                const int lim = (CAUSAL ? min(row, N - 1) : N - 1) - t0 - 16 * h;
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const uint32_t m = (uint32_t)((lim - (32 * kt + r)) >> 31);
+                        const float sv = s[kt][r];
+                        const uint32_t x = __float_as_uint(sv);
+                        s[kt][r] = __uint_as_float((x & ~m) | (0xFF800000u & m));
+                    }
+            }
+            // row maximum: one independent chain per 32-key tile, then the tiles,
+            // then the two lane halves (a maximum is exact in any order)
+            float mk[KT];
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                float a = s[kt][0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r)
+                    a = fmax_f(a, s[kt][r]);
+                mk[kt] = a;
+            }
+            float mx = mk[0];
+#pragma unroll
+            for (int kt = 1; kt < KT; ++kt)
+                mx = fmax_f(mx, mk[kt]);
+            mx = halves_max(mx);
+            const float m_new = fmax_f(m_run, mx);
+            const float mc_new = m_new * c;
+            const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
+            const float nmc = -mc_new;
+            // The rest is organised in stages so that no instruction waits on the
+            // result of the one just before it (this phase runs alone on its
+            // SIMD's vector ALU while the partner wave drives the matrix core):
+            // (1) x = fma(D, c, -mc) for all keys, in place;
+            // (2) P = exp2(x) for all keys, in place, interleaved with the rescale
+            //     of O (independent work for the vector ALU while exp2 is in flight);
+            // (3) l from the pre-cast P (one partial sum per tile), E4M3 cast.
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
-        }
-        __builtin_amdgcn_sched_barrier(0);
-        float lpart[KT];
+                    s[kt][r] = __builtin_fmaf(s[kt][r], c, nmc);
+            __builtin_amdgcn_sched_barrier(0);
+            // rescale O before this block's P.V; skipped when no row of the wave
+            // moved its maximum (alpha is then exactly 1)
+            const bool rescale = __ballot(alpha != 1.0f) != 0;
+            if (rescale) {
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) {
-            float l0 = s[kt][0] + s[kt][1], l1 = s[kt][2] + s[kt][3];
+                for (int t = 0; t < DT; ++t)
 #pragma unroll
-            for (int r = 4; r < 16; r += 4) {
-                l0 += s[kt][r] + s[kt][r + 1];
-                l1 += s[kt][r + 2] + s[kt][r + 3];
+                    for (int r = 0; r < 16; ++r)
+                        o[t][r] *= alpha;
             }
-            lpart[kt] = l0 + l1;
-        }
+            {
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt) {
+                for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
-                const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
-                uint32_t word;
-                // The first convert writes the low half of the word, the second
-                // the high half; the stale bytes of the previous block that the
-                // word starts from are all overwritten (no zeroing needed).
-                if constexpr (POW2) {
-                    s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
-                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, inv_S, false);
-                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, inv_S, true);
-                    word = __builtin_bit_cast(uint32_t, lo);
-                } else {
-                    const float y0 = __builtin_fminf(p0 * S, 448.f);
-                    const float y1 = __builtin_fminf(p1 * S, 448.f);
-                    const float y2 = __builtin_fminf(p2 * S, 448.f);
-                    const float y3 = __builtin_fminf(p3 * S, 448.f);
-                    int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)pk[kt][r4], false);
-                    wv = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, wv, true);
-                    word = (uint32_t)wv;
+                    for (int r = 0; r < 16; ++r)
+                        s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            float lpart[KT];
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                float l0 = s[kt][0] + s[kt][1], l1 = s[kt][2] + s[kt][3];
+#pragma unroll
+                for (int r = 4; r < 16; r += 4) {
+                    l0 += s[kt][r] + s[kt][r + 1];
+                    l1 += s[kt][r + 2] + s[kt][r + 3];
                 }
-                pk[kt][r4] = word;
-                if (COUNT) {
+                lpart[kt] = l0 + l1;
+            }
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
-                        const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < N &&
-                                       (!CAUSAL || key <= row);
-                        if (z) {
-                            if (j > 0) ++cnt2;
-                            else if (key < p.n_sink) ++cnt0;
-                            else ++cnt1;
+            for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
+                    const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
+                    uint32_t word;
+                    // The first convert writes the low half of the word, the second
+                    // the high half; the stale bytes of the previous block that the
+                    // word starts from are all overwritten (no zeroing needed).
+                    if constexpr (POW2) {
+                        s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, inv_S, false);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, inv_S, true);
+                        word = __builtin_bit_cast(uint32_t, lo);
+                    } else {
+                        const float y0 = __builtin_fminf(p0 * S, 448.f);
+                        const float y1 = __builtin_fminf(p1 * S, 448.f);
+                        const float y2 = __builtin_fminf(p2 * S, 448.f);
+                        const float y3 = __builtin_fminf(p3 * S, 448.f);
+                        int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)pk[kt][r4], false);
+                        wv = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, wv, true);
+                        word = (uint32_t)wv;
+                    }
+                    pk[kt][r4] = word;
+                    if (COUNT) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
+                            const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < N &&
+                                           (!CAUSAL || key <= row);
+                            if (z) {
+                                if (j > 0) ++cnt2;
+                                else if (key < p.n_sink) ++cnt0;
+                                else ++cnt1;
+                            }
                         }
                     }
                 }
             }
-        }
-        float lsum = lpart[0];
+            float lsum = lpart[0];
 #pragma unroll
-        for (int kt = 1; kt < KT; ++kt)
-            lsum += lpart[kt];
-        ell = alpha * ell + lsum;
-        m_run = m_new;
-        mc_run = mc_new;
-    };
+            for (int kt = 1; kt < KT; ++kt)
+                lsum += lpart[kt];
+            ell = alpha * ell + lsum;
+            m_run = m_new;
+            mc_run = mc_new;
+        };
 
-    // ---- prologue: K of the first block into stage 0 ----
-    if (grp == 0)
-        load_k(Ks0, jof(0));
-    // Q fragments and the first K stage are complete after this point; the
-    // compiler sees the wait (it tracks no outstanding loads in the loop)
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // Both groups run the same program -- per block k an MFMA phase (P.V of
-    // block k-1, S^T of block k) and a VALU phase (softmax of block k), each
-    // closed by a workgroup barrier -- but group 1 first passes one extra
-    // barrier, so it runs one phase behind group 0: while one wave of a SIMD
-    // is in its MFMA phase the other is in its softmax phase.  Group 0 issues
-    // the loads of K_{k+1} and V_k at the start of its MFMA phase k; they are
-    // first read two phases later.  Stage parity is k % 2 (the loop is
-    // unrolled twice so every LDS access names its stage statically).
-    if (grp == 1)
-        __syncthreads();
-    auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
-        __attribute__((always_inline)) {
-        if (grp == 0) {
-            if (k + 1 < nb)
-                load_k(k_nxt, jof(k + 1));
-            if (k < nb)
-                load_v(v_cur, jof(k));
-        }
-        if (valid(k - 1))
-            pv(v_prv);
-        if (valid(k))
-            qk(k_cur);
-        __syncthreads();
-        if (valid(k))
-            softmax(jof(k));
-        // the stage loads issued in the MFMA phase must land before the
-        // barrier that hands them to the next MFMA phase
+        // ---- prologue: K of the first block into stage 0 ----
         if (grp == 0)
-            wait_loads();
+            load_k(Ks0, jof(0));
+        // Q fragments and the first K stage are complete after this point; the
+        // compiler sees the wait (it tracks no outstanding loads in the loop)
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
-    };
-    for (int k = 0; k <= nb; k += 2) {
-        iteration(k, Ks0, Ks1, Vs0, Vs1);
-        if (k + 1 <= nb)
-            iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
-    }
-    if (grp == 0)
-        __syncthreads();
-
-    if (!wave_on)
-        return;
-    const float ell_row = ell + other_half(ell);
-    if (COUNT) {
-        cnt0 += other_half_u32(cnt0);
-        cnt1 += other_half_u32(cnt1);
-        cnt2 += other_half_u32(cnt2);
-    }
-    if (row < N) {
-        const size_t flat = (size_t)bh * N + row;
-        if (p.out) {
-            const float inv = 1.0f / (S * ell_row);
-            float* orow = p.out + flat * D;
-#pragma unroll
-            for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-                for (int r4 = 0; r4 < 4; ++r4) {
-                    f32x4 v4;
-                    v4[0] = o[dt][4 * r4 + 0] * inv;
-                    v4[1] = o[dt][4 * r4 + 1] * inv;
-                    v4[2] = o[dt][4 * r4 + 2] * inv;
-                    v4[3] = o[dt][4 * r4 + 3] * inv;
-                    *reinterpret_cast<f32x4*>(orow + 32 * dt + 8 * r4 + 4 * h) = v4;
-                }
+        // Both groups run the same program -- per block k an MFMA phase (P.V of
+        // block k-1, S^T of block k) and a VALU phase (softmax of block k), each
+        // closed by a workgroup barrier -- but group 1 first passes one extra
+        // barrier, so it runs one phase behind group 0: while one wave of a SIMD
+        // is in its MFMA phase the other is in its softmax phase.  Group 0 issues
+        // the loads of K_{k+1} and V_k at the start of its MFMA phase k; they are
+        // first read two phases later.  Stage parity is k % 2 (the loop is
+        // unrolled twice so every LDS access names its stage statically).
+        if (grp == 1)
+            __syncthreads();
+        auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
+            __attribute__((always_inline)) {
+            if (grp == 0) {
+                if (k + 1 < nb)
+                    load_k(k_nxt, jof(k + 1));
+                if (k < nb)
+                    load_v(v_cur, jof(k));
+            }
+            // the wave in its MFMA phase takes issue priority over its SIMD
+            // partner in the VALU phase, so the matrix core is fed first
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (valid(k - 1))
+                pv(v_prv);
+            if (valid(k))
+                qk(k_cur);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            if (valid(k))
+                softmax(jof(k));
+            // the stage loads issued in the MFMA phase must land before the
+            // barrier that hands them to the next MFMA phase
+            if (grp == 0)
+                wait_loads();
+            __syncthreads();
+        };
+        for (int k = 0; k <= nb; k += 2) {
+            iteration(k, Ks0, Ks1, Vs0, Vs1);
+            if (k + 1 <= nb)
+                iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
         }
-        if (h == 0) {
-            if (p.lse)
-                p.lse[flat] = (mc_run + log2f(ell_row)) * 0.69314718055994531f;
-            if (COUNT) {
-                p.counts[3 * flat + 0] = cnt0;
-                p.counts[3 * flat + 1] = cnt1;
-                p.counts[3 * flat + 2] = cnt2;
+        if (grp == 0)
+            __syncthreads();
+
+        if (!wave_on)
+            continue;
+        const float ell_row = ell + other_half(ell);
+        if (COUNT) {
+            cnt0 += other_half_u32(cnt0);
+            cnt1 += other_half_u32(cnt1);
+            cnt2 += other_half_u32(cnt2);
+        }
+        if (row < N) {
+            const size_t flat = (size_t)bh * N + row;
+            if (p.out) {
+                const float inv = 1.0f / (S * ell_row);
+                float* orow = p.out + flat * D;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        f32x4 v4;
+                        v4[0] = o[dt][4 * r4 + 0] * inv;
+                        v4[1] = o[dt][4 * r4 + 1] * inv;
+                        v4[2] = o[dt][4 * r4 + 2] * inv;
+                        v4[3] = o[dt][4 * r4 + 3] * inv;
+                        *reinterpret_cast<f32x4*>(orow + 32 * dt + 8 * r4 + 4 * h) = v4;
+                    }
+            }
+            if (h == 0) {
+                if (p.lse)
+                    p.lse[flat] = (mc_run + log2f(ell_row)) * 0.69314718055994531f;
+                if (COUNT) {
+                    p.counts[3 * flat + 0] = cnt0;
+                    p.counts[3 * flat + 1] = cnt1;
+                    p.counts[3 * flat + 2] = cnt2;
+                }
             }
         }
-    }
+    }  // tile of the pair
+    }  // unit
 }
 
 template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2>
-static hipError_t launch_one(const Params& p, hipStream_t stream)
+static hipError_t launch_one(const Params& p, int grid, hipStream_t stream)
 {
-    const int grid = p.per_xcd * kNumXcd;
     hipLaunchKernelGGL((fast_kernel<D, BC, CAUSAL, COUNT, POW2>), dim3(grid), dim3(512), 0, stream, p);
     return hipGetLastError();
 }
 
 template <int D, int BC>
-static hipError_t launch_d_bc(const Params& p, bool causal, bool count, bool pow2, hipStream_t s)
+static hipError_t launch_d_bc(const Params& p, int g, bool causal, bool count, bool pow2, hipStream_t s)
 {
     if (causal) {
-        if (count) return pow2 ? launch_one<D, BC, true, true, true>(p, s) : launch_one<D, BC, true, true, false>(p, s);
-        return pow2 ? launch_one<D, BC, true, false, true>(p, s) : launch_one<D, BC, true, false, false>(p, s);
+        if (count) return pow2 ? launch_one<D, BC, true, true, true>(p, g, s) : launch_one<D, BC, true, true, false>(p, g, s);
+        return pow2 ? launch_one<D, BC, true, false, true>(p, g, s) : launch_one<D, BC, true, false, false>(p, g, s);
     }
-    if (count) return pow2 ? launch_one<D, BC, false, true, true>(p, s) : launch_one<D, BC, false, true, false>(p, s);
-    return pow2 ? launch_one<D, BC, false, false, true>(p, s) : launch_one<D, BC, false, false, false>(p, s);
+    if (count) return pow2 ? launch_one<D, BC, false, true, true>(p, g, s) : launch_one<D, BC, false, true, false>(p, g, s);
+    return pow2 ? launch_one<D, BC, false, false, true>(p, g, s) : launch_one<D, BC, false, false, false>(p, g, s);
 }
 
-hipError_t launch_fast(const Params& p, int d, int block_kv, bool causal, bool count,
+hipError_t launch_fast(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
                        bool pow2_scale, hipStream_t stream)
 {
     if (d == 64)
-        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, pow2_scale, stream)
-                              : launch_d_bc<64, 128>(p, causal, count, pow2_scale, stream);
-    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, pow2_scale, stream)
-                          : launch_d_bc<128, 128>(p, causal, count, pow2_scale, stream);
+        return block_kv == 64 ? launch_d_bc<64, 64>(p, grid, causal, count, pow2_scale, stream)
+                              : launch_d_bc<64, 128>(p, grid, causal, count, pow2_scale, stream);
+    return block_kv == 64 ? launch_d_bc<128, 64>(p, grid, causal, count, pow2_scale, stream)
+                          : launch_d_bc<128, 128>(p, grid, causal, count, pow2_scale, stream);
 }
 
 int fast_rows_per_wg(int, int) { return 256; }

@@ -77,6 +77,8 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.n_tiles = (int)n_tiles;
     p.total_wg = (int)total;
     p.per_xcd = (int)((total + attn::kNumXcd - 1) / attn::kNumXcd);
+    p.pairs = (int)((n_tiles + 1) / 2);
+    p.units = (long long)B * Hq * p.pairs;
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
@@ -84,7 +86,16 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
         const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
-        e = attn::launch_fast(p, d, block_kv, causal != 0, count, pow2, s);
+        // persistent grid: one workgroup per CU (the LDS footprint admits no
+        // second one), 8 XCDs, never more workgroups than work units
+        int dev = 0, n_cu = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return ATTN_ERR_HIP;
+        const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
+        const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
+                                                                            : per_xcd_max;
+        e = attn::launch_fast(p, (int)(per_xcd * attn::kNumXcd), d, block_kv, causal != 0, count, pow2, s);
     } else {
         e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, s);
     }
