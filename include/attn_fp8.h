@@ -69,6 +69,21 @@ enum {
     ATTN_MODE_NOCAST = 2
 };
 
+/*
+ * Flag OR-ed into `mode`: dynamic per-block power-of-two P-scale (the
+ * paper's Limitations and Future Work proposes scaling each block by a power
+ * of two chosen from its own P range, without fixing the rule).  Rule used
+ * here: S must be 2^k0 with 0 <= k0 <= 8; block j of query row r casts
+ * P * 2^kj with
+ *   kj = k0 + clamp(floor(-xmax), 0, 126 - k0),  xmax = fma(mloc, c, -mc),
+ * mloc the block's largest raw score of the row and mc = fl(m_new c), so the
+ * block's largest P lands in (S/2, S] like P = 1 does under the static S; a
+ * block holding the running maximum keeps kj = k0.  The cast value is taken
+ * back to S units exactly (times 2^(k0 - kj)), so l, O and the epilogue are
+ * those of the static scale.  With ATTN_MODE_NOCAST the flag changes nothing.
+ */
+enum { ATTN_SCALE_DYNAMIC = 0x100 };
+
 enum {
     ATTN_ORDER_FORWARD = 0, /* KV blocks 0, 1, ..., last (sink block first)  */
     ATTN_ORDER_REVERSE = 1  /* KV blocks last, ..., 1, 0 (sink block last)   */
@@ -96,7 +111,7 @@ enum {
  *   order     ATTN_ORDER_FORWARD or ATTN_ORDER_REVERSE.
  *   S         static P-scale (Sec. 5), finite and > 0.  Powers of two make the
  *             scaling exact (Prop. 2); S = 256 is the paper's choice.
- *   mode      ATTN_MODE_*.
+ *   mode      ATTN_MODE_*, optionally OR ATTN_SCALE_DYNAMIC.
  *   stream    hipStream_t or NULL.
  * Returns ATTN_OK or an ATTN_ERR_* code.
  */

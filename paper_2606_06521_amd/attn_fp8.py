@@ -19,9 +19,11 @@ LIB_PATH = os.path.join(_HERE, "libattn_fp8.so")
 ATTN_MODE_FAITHFUL, ATTN_MODE_FAST, ATTN_MODE_NOCAST = 0, 1, 2
 ATTN_ORDER_FORWARD, ATTN_ORDER_REVERSE = 0, 1
 ATTN_OK, ATTN_ERR_INVALID_ARG, ATTN_ERR_UNSUPPORTED, ATTN_ERR_HIP = 0, -1, -2, -3
+ATTN_SCALE_DYNAMIC = 0x100
 
 MODES = {"faithful": ATTN_MODE_FAITHFUL, "fast": ATTN_MODE_FAST, "nocast": ATTN_MODE_NOCAST}
 ORDERS = {"forward": ATTN_ORDER_FORWARD, "reverse": ATTN_ORDER_REVERSE}
+SCALES = {"static": 0, "dynamic": ATTN_SCALE_DYNAMIC}
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -100,8 +102,9 @@ def _stream(stream):
 
 def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
         block_kv: int = 128, mode: str = "fast", out=None, lse=None, want_lse: bool = True,
-        stream=None):
-    """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None)."""
+        stream=None, scale: str = "static"):
+    """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None).
+    scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8)."""
     m = MODES[mode]
     B, Hq, Hkv, N, d = _check(q, k, v, m)
     if out is None:
@@ -109,7 +112,8 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
     st = attn_fp8_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N, d,
-                      int(bool(causal)), int(block_kv), ORDERS[order], S, m, _stream(stream))
+                      int(bool(causal)), int(block_kv), ORDERS[order], S, m | SCALES[scale],
+                      _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return out, lse
@@ -117,13 +121,14 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
 
 def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
                       block_kv: int = 128, mode: str = "fast", n_sink: int = 4, out=None, lse=None,
-                      stream=None):
+                      stream=None, scale: str = "static"):
     """P-underflow diagnostic; returns counts [B,Hq,N,3] uint32 (as int32 storage)."""
     m = MODES[mode]
     B, Hq, Hkv, N, d = _check(q, k, v, m)
     counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
     st = attn_fp8_p_underflow_count(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d,
-                                    int(bool(causal)), int(block_kv), ORDERS[order], S, m,
+                                    int(bool(causal)), int(block_kv), ORDERS[order], S,
+                                    m | SCALES[scale],
                                     int(n_sink), _ptr(counts), _ptr(out), _ptr(lse),
                                     _stream(stream))
     if st != ATTN_OK:

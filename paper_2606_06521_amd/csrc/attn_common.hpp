@@ -37,8 +37,9 @@ struct Params {
     int B, Hq, Hkv, N;
     int order;           // 0 forward, 1 reverse
     int n_sink;
-    float S;             // static P-scale
+    float S;             // static P-scale (2^k0 with the dynamic scale)
     float inv_S;         // 1/S, used only when S is a power of two (exact)
+    int k0;              // log2 S (dynamic scale only)
     float c;             // fl32(log2(e) / sqrt(d))
     int n_tiles;         // query tiles per (batch, head)
     int total_wg;        // B * Hq * n_tiles
@@ -48,6 +49,11 @@ struct Params {
     int pairs;           // units per (batch, head) = ceil(n_tiles / 2)
     long long units;     // B * Hq * pairs
 };
+
+// how the fast kernel applies the P-scale
+constexpr int kScaleAny = 0;       // static S: multiply, clamp at 448, convert
+constexpr int kScalePow2 = 1;      // static S = 2^k <= 256: the scaled convert
+constexpr int kScaleDynamic = 2;   // per-block 2^kj (S = 2^k0 its floor)
 
 constexpr int kNumXcd = 8;   // MI355X: 8 XCDs x 32 CUs, workgroup i runs on XCD i % 8
 

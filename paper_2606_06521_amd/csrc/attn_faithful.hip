@@ -6,7 +6,8 @@
 // in FP64 and rounded once to FP32; P*S goes through the hardware E4M3
 // convert (round to nearest even) and straight back through the hardware
 // decode, so the P.V operand holds the exact E4M3 values.  ATTN_MODE_NOCAST
-// (CAST = false) skips the convert.
+// (CAST = false) skips the convert.  DYN: the dynamic per-block power-of-two
+// scale (the cast of each block uses 2^kj instead of S).
 //
 // This mode exists for parity and precision studies, not speed: K_j and V_j
 // are staged through LDS once per block with no prefetch.
@@ -17,7 +18,7 @@
 
 namespace attn {
 
-template <int D, int BC, bool CAUSAL, bool COUNT, bool CAST>
+template <int D, int BC, bool CAUSAL, bool COUNT, bool CAST, bool DYN>
 __global__ void __launch_bounds__(256) faithful_kernel(Params p)
 {
     constexpr int NW = 4;
@@ -151,6 +152,17 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
         const float mc_new = m_new * c;
         const float alpha = (float)exp2((double)(mc_run - mc_new));
         const float nmc = -mc_new;
+        // Dynamic P-scale: this block's rows cast P * 2^kj, kj = k0 +
+        // clamp(floor(-xmax), 0, 126 - k0) with xmax = fma(block max, c, -mc),
+        // and the decoded value goes back to S units times 2^(k0 - kj) (exact)
+        float Sj = S, back = 1.f;
+        if (DYN) {
+            const float xmax = __builtin_fmaf(mx, c, nmc);
+            const float f = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(-xmax), 0.f), (float)(126 - p.k0));
+            const int kj = p.k0 + (int)f;
+            Sj = __uint_as_float((uint32_t)(127 + kj) << 23);
+            back = __uint_as_float((uint32_t)(127 + p.k0 - kj) << 23);
+        }
 
         // ---- P = exp(Z - m_new); l from pre-cast P; P~ = E4M3(P*S) ----
         float lsum = 0.f;
@@ -165,8 +177,8 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
                 const float p1 = (float)exp2((double)x1);
                 lsum += p0;
                 lsum += p1;
-                float y0 = p0 * S;
-                float y1 = p1 * S;
+                float y0 = p0 * Sj;
+                float y1 = p1 * Sj;
                 if (CAST) {
                     // saturate at the largest finite E4M3 value before the convert
                     y0 = __builtin_fminf(y0, 448.f);
@@ -186,6 +198,10 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
                     const auto dec = __builtin_amdgcn_cvt_pk_f32_fp8(code, false);
                     y0 = dec[0];
                     y1 = dec[1];
+                }
+                if (DYN) {
+                    y0 *= back;
+                    y1 *= back;
                 }
                 pt[kt][r] = y0;
                 pt[kt][r + 1] = y1;
@@ -251,11 +267,11 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
     }
 }
 
-template <int D, int BC, bool CAUSAL, bool COUNT, bool CAST>
+template <int D, int BC, bool CAUSAL, bool COUNT, bool CAST, bool DYN>
 static hipError_t launch_one(const Params& p, hipStream_t stream)
 {
     constexpr size_t lds = sizeof(float) * (size_t)BC * ((D + 4) + D);
-    auto kern = faithful_kernel<D, BC, CAUSAL, COUNT, CAST>;
+    auto kern = faithful_kernel<D, BC, CAUSAL, COUNT, CAST, DYN>;
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess)
@@ -265,25 +281,33 @@ static hipError_t launch_one(const Params& p, hipStream_t stream)
     return hipGetLastError();
 }
 
-template <int D, int BC>
-static hipError_t launch_d_bc(const Params& p, bool causal, bool count, bool cast, hipStream_t s)
+template <int D, int BC, bool CAUSAL, bool COUNT>
+static hipError_t launch_cast(const Params& p, bool cast, bool dyn, hipStream_t s)
 {
-    if (causal) {
-        if (count) return cast ? launch_one<D, BC, true, true, true>(p, s) : launch_one<D, BC, true, true, false>(p, s);
-        return cast ? launch_one<D, BC, true, false, true>(p, s) : launch_one<D, BC, true, false, false>(p, s);
-    }
-    if (count) return cast ? launch_one<D, BC, false, true, true>(p, s) : launch_one<D, BC, false, true, false>(p, s);
-    return cast ? launch_one<D, BC, false, false, true>(p, s) : launch_one<D, BC, false, false, false>(p, s);
+    if (!cast)
+        return launch_one<D, BC, CAUSAL, COUNT, false, false>(p, s);
+    return dyn ? launch_one<D, BC, CAUSAL, COUNT, true, true>(p, s)
+               : launch_one<D, BC, CAUSAL, COUNT, true, false>(p, s);
 }
 
+template <int D, int BC>
+static hipError_t launch_d_bc(const Params& p, bool causal, bool count, bool cast, bool dyn, hipStream_t s)
+{
+    if (causal)
+        return count ? launch_cast<D, BC, true, true>(p, cast, dyn, s) : launch_cast<D, BC, true, false>(p, cast, dyn, s);
+    return count ? launch_cast<D, BC, false, true>(p, cast, dyn, s) : launch_cast<D, BC, false, false>(p, cast, dyn, s);
+}
+
+// Without the cast the dynamic scale is the static one (P * 2^kj * 2^(k0-kj)
+// = P * S exactly), so ATTN_MODE_NOCAST ignores it.
 hipError_t launch_faithful(const Params& p, int d, int block_kv, bool causal, bool count,
-                           bool cast, hipStream_t stream)
+                           bool cast, bool dynamic, hipStream_t stream)
 {
     if (d == 64)
-        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, cast, stream)
-                              : launch_d_bc<64, 128>(p, causal, count, cast, stream);
-    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, cast, stream)
-                          : launch_d_bc<128, 128>(p, causal, count, cast, stream);
+        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, cast, dynamic, stream)
+                              : launch_d_bc<64, 128>(p, causal, count, cast, dynamic, stream);
+    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, cast, dynamic, stream)
+                          : launch_d_bc<128, 128>(p, causal, count, cast, dynamic, stream);
 }
 
 int faithful_rows_per_wg() { return 128; }

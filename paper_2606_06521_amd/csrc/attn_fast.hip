@@ -6,7 +6,9 @@
 //   m, alpha, P, l       per-lane scalars (one query row per lane)
 //   P8 = E4M3(P * S)     v_cvt_pk_fp8_f32 (round to nearest even); for S = 2^k
 //                        the scaled convert v_cvt_scalef32_pk_fp8_f32 applies
-//                        the exact power-of-two scale inside the convert
+//                        the exact power-of-two scale inside the convert; the
+//                        dynamic per-block scale 2^kj rides on the same convert
+//                        (per-lane scale) and on the P.V MFMA's E8M0 B scale
 //   O^T += V_j^T P8^T    v_mfma_f32_32x32x64_f8f6f4 (E4M3 x E4M3), FP32 accumulate
 //   out = O / (S l)
 //
@@ -70,7 +72,9 @@ __device__ inline i32x2 lds_read_tr8(const uint8_t* p)
 
 }  // namespace
 
-template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2>
+// SCALE: kScaleAny (static S, multiply and convert), kScalePow2 (static
+// S = 2^k, the scaled convert) or kScaleDynamic (per-block 2^kj, see softmax).
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE>
 __global__ void __launch_bounds__(512) fast_kernel(Params p)
 {
     constexpr int NW = 8;
@@ -236,6 +240,9 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                 o[dt][r] = 0.f;
         f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
         uint32_t pk[KT][4] = {};      // E4M3 P bytes between the VALU and the next MFMA phase
+        // dynamic scale: E8M0 byte 127 + k0 - kj of each row's block, the P.V
+        // MFMA's B-operand scale, which takes the block back to S units
+        int pv_sb = 127;
         uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
 
         // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
@@ -304,7 +311,12 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                     bop[4 + q4] = (int)pk[2 * js + 1][q4];
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0, 0, 0, 0);
+                if constexpr (SCALE == kScaleDynamic)
+                    o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0,
+                                                                            127, 0, pv_sb);
+                else
+                    o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0,
+                                                                            0, 0, 0);
                 __builtin_amdgcn_sched_barrier(0);
             }
         };
@@ -346,6 +358,19 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             const float mc_new = m_new * c;
             const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
             const float nmc = -mc_new;
+            // Dynamic P-scale (Limitations and Future Work, read as: the
+            // block's largest P lands in (S/2, S]): kj = k0 + clamp(floor(-xmax),
+            // 0, 126 - k0), xmax = fma(block max, c, -mc).  The convert scales
+            // by 2^kj (scale operand 2^-kj) and P.V by 2^(k0 - kj).
+            float cvt_scale = inv_S;
+            if constexpr (SCALE == kScaleDynamic) {
+                const float xmax = __builtin_fmaf(mx, c, nmc);
+                const float f = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(-xmax), 0.f),
+                                                (float)(126 - p.k0));
+                const int kj = p.k0 + (int)f;
+                cvt_scale = __uint_as_float((uint32_t)(127 - kj) << 23);
+                pv_sb = 127 + p.k0 - kj;
+            }
             // The rest is organised in stages so that no instruction waits on the
             // result of the one just before it (this phase runs alone on its
             // SIMD's vector ALU while the partner wave drives the matrix core):
@@ -398,10 +423,10 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                     // The first convert writes the low half of the word, the second
                     // the high half; the stale bytes of the previous block that the
                     // word starts from are all overwritten (no zeroing needed).
-                    if constexpr (POW2) {
+                    if constexpr (SCALE != kScaleAny) {
                         s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
-                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, inv_S, false);
-                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, inv_S, true);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, cvt_scale, false);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, cvt_scale, true);
                         word = __builtin_bit_cast(uint32_t, lo);
                     } else {
                         const float y0 = __builtin_fminf(p0 * S, 448.f);
@@ -530,32 +555,39 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     }  // unit
 }
 
-template <int D, int BC, bool CAUSAL, bool COUNT, bool POW2>
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE>
 static hipError_t launch_one(const Params& p, int grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((fast_kernel<D, BC, CAUSAL, COUNT, POW2>), dim3(grid), dim3(512), 0, stream, p);
+    hipLaunchKernelGGL((fast_kernel<D, BC, CAUSAL, COUNT, SCALE>), dim3(grid), dim3(512), 0, stream, p);
     return hipGetLastError();
 }
 
-template <int D, int BC>
-static hipError_t launch_d_bc(const Params& p, int g, bool causal, bool count, bool pow2, hipStream_t s)
+template <int D, int BC, bool CAUSAL, bool COUNT>
+static hipError_t launch_scale(const Params& p, int g, int scale, hipStream_t s)
 {
-    if (causal) {
-        if (count) return pow2 ? launch_one<D, BC, true, true, true>(p, g, s) : launch_one<D, BC, true, true, false>(p, g, s);
-        return pow2 ? launch_one<D, BC, true, false, true>(p, g, s) : launch_one<D, BC, true, false, false>(p, g, s);
-    }
-    if (count) return pow2 ? launch_one<D, BC, false, true, true>(p, g, s) : launch_one<D, BC, false, true, false>(p, g, s);
-    return pow2 ? launch_one<D, BC, false, false, true>(p, g, s) : launch_one<D, BC, false, false, false>(p, g, s);
+    if (scale == kScaleDynamic)
+        return launch_one<D, BC, CAUSAL, COUNT, kScaleDynamic>(p, g, s);
+    if (scale == kScalePow2)
+        return launch_one<D, BC, CAUSAL, COUNT, kScalePow2>(p, g, s);
+    return launch_one<D, BC, CAUSAL, COUNT, kScaleAny>(p, g, s);
+}
+
+template <int D, int BC>
+static hipError_t launch_d_bc(const Params& p, int g, bool causal, bool count, int scale, hipStream_t s)
+{
+    if (causal)
+        return count ? launch_scale<D, BC, true, true>(p, g, scale, s) : launch_scale<D, BC, true, false>(p, g, scale, s);
+    return count ? launch_scale<D, BC, false, true>(p, g, scale, s) : launch_scale<D, BC, false, false>(p, g, scale, s);
 }
 
 hipError_t launch_fast(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
-                       bool pow2_scale, hipStream_t stream)
+                       int scale, hipStream_t stream)
 {
     if (d == 64)
-        return block_kv == 64 ? launch_d_bc<64, 64>(p, grid, causal, count, pow2_scale, stream)
-                              : launch_d_bc<64, 128>(p, grid, causal, count, pow2_scale, stream);
-    return block_kv == 64 ? launch_d_bc<128, 64>(p, grid, causal, count, pow2_scale, stream)
-                          : launch_d_bc<128, 128>(p, grid, causal, count, pow2_scale, stream);
+        return block_kv == 64 ? launch_d_bc<64, 64>(p, grid, causal, count, scale, stream)
+                              : launch_d_bc<64, 128>(p, grid, causal, count, scale, stream);
+    return block_kv == 64 ? launch_d_bc<128, 64>(p, grid, causal, count, scale, stream)
+                          : launch_d_bc<128, 128>(p, grid, causal, count, scale, stream);
 }
 
 int fast_rows_per_wg(int, int) { return 256; }

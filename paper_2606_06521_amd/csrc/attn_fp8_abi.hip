@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kVersion = 100;   // 0.1.0
+constexpr int kVersion = 200;   // 0.2.0: dynamic per-block scale
 
 bool is_pow2_scale(float S)
 {
@@ -22,8 +22,10 @@ bool is_pow2_scale(float S)
 // Shared validation and dispatch of both entry points.
 int run(const void* q, const void* k, const void* v, float* out, float* lse,
         uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int d, int causal,
-        int block_kv, int order, float S, int mode, int n_sink, void* stream)
+        int block_kv, int order, float S, int mode_flags, int n_sink, void* stream)
 {
+    const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
+    const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
     if (B < 0 || Hq < 1 || Hkv < 1 || N < 0 || Hq % Hkv != 0)
         return ATTN_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1)
@@ -36,6 +38,15 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     if (n_sink < 0)
         return ATTN_ERR_INVALID_ARG;
+    // the dynamic scale keeps S = 2^k0 as its floor, 0 <= k0 <= 8
+    int k0 = 0;
+    if (dyn) {
+        int e = 0;
+        const float f = frexpf(S, &e);
+        k0 = e - 1;
+        if (f != 0.5f || k0 < 0 || k0 > 8)
+            return ATTN_ERR_INVALID_ARG;
+    }
     if (d < 1 || block_kv < 1)
         return ATTN_ERR_INVALID_ARG;
     if (d != 64 && d != 128)
@@ -72,6 +83,7 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.n_sink = n_sink;
     p.S = S;
     p.inv_S = 1.0f / S;
+    p.k0 = k0;
     // exp(z) = exp2(D * c) with z = D / sqrt(d): c rounded once from double
     p.c = (float)(1.4426950408889634074 / sqrt((double)d));
     p.n_tiles = (int)n_tiles;
@@ -86,6 +98,7 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
         const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
+        const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
         // persistent grid: one workgroup per CU (the LDS footprint admits no
         // second one), 8 XCDs, never more workgroups than work units
         int dev = 0, n_cu = 0;
@@ -95,9 +108,9 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
         const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
                                                                             : per_xcd_max;
-        e = attn::launch_fast(p, (int)(per_xcd * attn::kNumXcd), d, block_kv, causal != 0, count, pow2, s);
+        e = attn::launch_fast(p, (int)(per_xcd * attn::kNumXcd), d, block_kv, causal != 0, count, scale, s);
     } else {
-        e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, s);
+        e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, dyn, s);
     }
     return e == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
@@ -130,7 +143,8 @@ const char* attn_fp8_strerror(int status)
         return "ok";
     case ATTN_ERR_INVALID_ARG:
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
-               "and positive, or order/mode/causal/n_sink out of range)";
+               "and positive, or order/mode/causal/n_sink out of range; the dynamic scale "
+               "needs S = 2^k with 0 <= k <= 8)";
     case ATTN_ERR_UNSUPPORTED:
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:

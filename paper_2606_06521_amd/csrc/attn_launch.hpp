@@ -7,12 +7,12 @@
 namespace attn {
 
 hipError_t launch_faithful(const Params& p, int d, int block_kv, bool causal, bool count,
-                           bool cast, hipStream_t stream);
+                           bool cast, bool dynamic, hipStream_t stream);
 int faithful_rows_per_wg();
 
 // grid: a multiple of 8 workgroups, at most one per CU (persistent kernel)
 hipError_t launch_fast(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
-                       bool pow2_scale, hipStream_t stream);
+                       int scale /* kScale* */, hipStream_t stream);
 int fast_rows_per_wg(int d, int block_kv);
 
 }  // namespace attn

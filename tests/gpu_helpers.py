@@ -30,14 +30,15 @@ def to_device(inp):
     return q, k, v
 
 
-def run_gpu(dev, mode, S, order, causal, block_kv, n_sink=4, counts=True):
+def run_gpu(dev, mode, S, order, causal, block_kv, n_sink=4, counts=True, scale="static"):
     from paper_2606_06521_amd import attn_fp8 as A
     q, k, v = dev
-    out, lse = A.fwd(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv, mode=mode)
+    out, lse = A.fwd(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv, mode=mode,
+                     scale=scale)
     cnt = None
     if counts:
         cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv,
-                                  mode=mode, n_sink=n_sink)
+                                  mode=mode, n_sink=n_sink, scale=scale)
     torch.cuda.synchronize()
     res = (out.cpu().numpy(), lse.cpu().numpy(), None if cnt is None else cnt.cpu().numpy().view(np.uint32))
     return res
@@ -48,7 +49,8 @@ def counts_are_exact(mode, S) -> bool:
     on identical P values: faithful mode (exp2 in FP64 on both sides, any S),
     and fast mode for S = 2^k, where the decision is the integer threshold
     x <= -(10 + k) and the hardware exp2 is exact at integers and monotone
-    around them (see test_gpu_probes)."""
+    around them (see test_gpu_probes).  The dynamic scale keeps that property:
+    block j's threshold is the integer x <= -(10 + kj)."""
     if mode == "faithful":
         return True
     if mode == "fast":
@@ -56,14 +58,15 @@ def counts_are_exact(mode, S) -> bool:
     return False
 
 
-def compare(inp, gpu, mode, S, order, causal, block_kv, rows=None, n_sink=4, label=""):
+def compare(inp, gpu, mode, S, order, causal, block_kv, rows=None, n_sink=4, label="",
+            scale="static"):
     """Oracle on `rows` (flat ids, None = all); asserts counts bit-exact (where
     claimed) and out / lse within tolerance.  Returns the measured differences."""
     out_g, lse_g, cnt_g = gpu
     d = inp.d
     o_out, o_lse, o_cnt = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,
                                       block_kv=block_kv, causal=causal, cast=(mode != "nocast"),
-                                      n_sink=n_sink, rows=rows)
+                                      n_sink=n_sink, rows=rows, scale=scale)
     g_out = out_g.reshape(-1, d)
     g_lse = lse_g.reshape(-1)
     if rows is not None:

@@ -4,7 +4,9 @@
 // oracle or with exact host arithmetic:
 //   - v_cvt_pk_fp8_f32 and v_cvt_scalef32_pk_fp8_f32 (the E4M3 P-cast),
 //   - v_exp_f32 (exp2 in the fast kernels),
-//   - the operand/accumulator lane layouts of the three MFMA shapes used.
+//   - the operand/accumulator lane layouts of the three MFMA shapes used,
+//   - the per-lane E8M0 operand scales of the block-scaled FP8 MFMA and the
+//     per-lane scale of the scaled convert (the dynamic P-scale).
 // Every kernel bounds-checks its index against n.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -103,6 +105,47 @@ __global__ void k_mfma_fp8(const uint8_t* A, const uint8_t* B, float* D)
         D[(8 * (r / 4) + 4 * h + (r % 4)) * 32 + m] = acc[r];
 }
 
+// One wave, the block-scaled FP8 MFMA.  As k_mfma_fp8, plus one E8M0 scale
+// byte per lane for A (sa[l]) and for B (sb[l]), passed in byte 0 of the
+// scale operands.  Assumed: lane (m, h)'s byte scales the 32 elements it
+// supplies, A[m][32h .. 32h+31] and B[32h .. 32h+31][m], by 2^(byte - 127).
+__global__ void k_mfma_fp8_scaled(const uint8_t* A, const uint8_t* B, const uint8_t* sa,
+                                  const uint8_t* sb, float* D)
+{
+    const int l = threadIdx.x;
+    if (l >= 64)
+        return;
+    const int m = l & 31, h = l >> 5;
+    i32x8 a, b;
+    for (int q = 0; q < 8; ++q) {
+        uint32_t wa = 0, wb = 0;
+        for (int e = 0; e < 4; ++e) {
+            const int kk = 32 * h + 4 * q + e;
+            wa |= (uint32_t)A[m * 64 + kk] << (8 * e);
+            wb |= (uint32_t)B[kk * 32 + m] << (8 * e);
+        }
+        a[q] = (int)wa;
+        b[q] = (int)wb;
+    }
+    f32x16 acc = {};
+    acc = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, acc, 0, 0, 0, (int)sa[l], 0, (int)sb[l]);
+    for (int r = 0; r < 16; ++r)
+        D[(8 * (r / 4) + 4 * h + (r % 4)) * 32 + m] = acc[r];
+}
+
+// The scaled convert with a per-element scale: out = cvt(x[i] / scale[i]) pairs.
+__global__ void k_cvt_scaled_vec(const float* x, const float* scale, int64_t n, uint8_t* out)
+{
+    const int64_t i = 2 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+    if (i + 1 >= n)
+        return;
+    s16x2 z = {0, 0};
+    // both elements of a pair share the scale of the first
+    const uint32_t w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(z, x[i], x[i + 1], scale[i], false));
+    out[i] = (uint8_t)(w & 0xFF);
+    out[i + 1] = (uint8_t)((w >> 8) & 0xFF);
+}
+
 // One wave.  A: 32x2 f32, B: 2x32 f32, D: 32x32 f32.  Lane (m, h): A[m][h], B[h][m].
 __global__ void k_mfma_f32(const float* A, const float* B, float* D)
 {
@@ -147,6 +190,25 @@ int probe_exp2(const float* x, int64_t n, float* out, void* stream)
     if (n <= 0 || !x || !out)
         return -1;
     hipLaunchKernelGGL(k_exp2, dim3(grid_for(n, 256)), dim3(256), 0, (hipStream_t)stream, x, n, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int probe_mfma_fp8_scaled(const uint8_t* A, const uint8_t* B, const uint8_t* sa, const uint8_t* sb,
+                          float* D, void* stream)
+{
+    if (!A || !B || !sa || !sb || !D)
+        return -1;
+    hipLaunchKernelGGL(k_mfma_fp8_scaled, dim3(1), dim3(64), 0, (hipStream_t)stream, A, B, sa, sb, D);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// n must be even (pairs)
+int probe_cvt_scaled_vec(const float* x, const float* scale, int64_t n, uint8_t* out, void* stream)
+{
+    if (n <= 0 || (n & 1) || !x || !scale || !out)
+        return -1;
+    hipLaunchKernelGGL(k_cvt_scaled_vec, dim3(grid_for(n / 2, 256)), dim3(256), 0, (hipStream_t)stream,
+                       x, scale, n, out);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -44,6 +44,49 @@ def test_small_fast(d, bkv, causal, order):
         compare(inp, gpu, "fast", S, order, causal, bkv, label=label)
 
 
+@pytest.mark.parametrize("d,bkv,causal,order", SMALL)
+def test_small_dynamic_scale(d, bkv, causal, order):
+    # dynamic per-block 2^kj scale in both modes: counts exact, outputs to the mode's bar
+    for mode, fmt in (("faithful", "f32"), ("fast", "bf16_e4m3")):
+        inp = make_inputs(2, 4, 2, 333, d, fmt=fmt, delta=10.0, seed=500 + d + bkv)
+        dev = to_device(inp)
+        for S in (1.0, 16.0, 256.0):
+            label = f"dynamic {mode} d={d} bkv={bkv} causal={causal} {order} S={S}"
+            log(label)
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale="dynamic")
+            compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale="dynamic")
+
+
+def test_dynamic_scale_sweep_rows_and_collapse():
+    # the Delta sweep (8 heads, N=4096, block 128) on sampled rows: parity, and
+    # the forward-order collapse of non-sink P gone (no zero code outside the
+    # sink's block at S = 256, as in reverse order)
+    w = WORKLOADS["sink_sweep_h8_n4096_d128_faithful"]
+    base = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=0.0, seed=w.seed_base)
+    rows = np.concatenate([np.arange(h * w.N, (h + 1) * w.N, 64) + (5 * h) % 64 for h in range(w.Hq)])
+    for D in (7.0, 12.0):
+        inp = with_delta(base, D)
+        dev = to_device(inp)
+        for order in w.orders:
+            label = f"{w.name} dynamic Delta={D} S=256 {order}"
+            log(label)
+            gpu = run_gpu(dev, w.mode, 256.0, order, w.causal, w.block_kv, scale="dynamic")
+            compare(inp, gpu, w.mode, 256.0, order, w.causal, w.block_kv, rows=rows, label=label,
+                    scale="dynamic")
+            assert gpu[2][..., 2].sum() == 0, label
+        del dev
+        torch.cuda.empty_cache()
+
+
+def test_dynamic_scale_rejects_non_power_of_two():
+    from paper_2606_06521_amd import attn_fp8 as A
+    inp = make_inputs(1, 2, 1, 64, 64, fmt="bf16_e4m3", delta=7.0, seed=7)
+    q, k, v = to_device(inp)
+    for S in (3.0, 512.0, 0.5):
+        with pytest.raises(A.AttnError):
+            A.fwd(q, k, v, S=S, mode="fast", scale="dynamic")
+
+
 @pytest.mark.parametrize("N", [1, 31, 32, 33, 64, 65, 129])
 @pytest.mark.parametrize("mode", ["faithful", "fast"])
 def test_edge_lengths(N, mode):

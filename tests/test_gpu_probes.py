@@ -139,3 +139,63 @@ def test_mfma_f32_layout(probes):
     D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
     assert probes.probe_mfma(2, At.data_ptr(), Bt.data_ptr(), D.data_ptr(), _stream()) == 0
     assert np.array_equal(D.cpu().numpy(), A @ B)
+
+
+def test_mfma_fp8_block_scales_per_lane(probes):
+    """Block scales of the FP8 MFMA (byte 0 of each lane's scale operand):
+    lane m + 32 g (g = 0, 1) scales row m of A (column m of B) at the K
+    positions k with (k mod 32) div 16 == g, i.e. the first 16 operand
+    elements of both lanes of the row take lane m's scale and the last 16
+    take lane m + 32's.  The dynamic P-scale gives both lanes of a query row
+    the same byte, so the whole column of P of that row is scaled by it."""
+    rng = np.random.default_rng(11)
+    A = rng.integers(-8, 9, (32, 64)).astype(np.float32) / 4
+    B = rng.integers(-8, 9, (64, 32)).astype(np.float32) / 8
+    sa = rng.integers(120, 135, 64).astype(np.uint8)
+    sb = rng.integers(100, 128, 64).astype(np.uint8)
+    k = np.arange(64)
+    g = (k % 32) // 16
+    As = A * np.exp2(sa[np.arange(32)[:, None] + 32 * g[None, :]].astype(np.float64) - 127)
+    Bs = B * np.exp2(sb[np.arange(32)[None, :] + 32 * g[:, None]].astype(np.float64) - 127)
+
+    def run(sa_, sb_):
+        Ac = torch.from_numpy(A).to(torch.float8_e4m3fn).view(torch.uint8).cuda()
+        Bc = torch.from_numpy(B).to(torch.float8_e4m3fn).view(torch.uint8).cuda()
+        sat, sbt = torch.from_numpy(sa_).cuda(), torch.from_numpy(sb_).cuda()
+        D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+        assert probes.probe_mfma_fp8_scaled(Ac.data_ptr(), Bc.data_ptr(), sat.data_ptr(),
+                                            sbt.data_ptr(), D.data_ptr(), _stream()) == 0
+        return D.cpu().numpy().astype(np.float64)
+
+    got = run(sa, sb)
+    want = As @ Bs
+    # FP32 accumulation of 64 terms: within 64 ulps of the sum of magnitudes
+    bound = (np.abs(As) @ np.abs(Bs)) * 64 * 2.0 ** -24
+    assert np.all(np.abs(got - want) <= bound), np.abs(got - want).max()
+    # the kernel's use: one byte per column of B, in both of its lanes
+    col = rng.integers(9, 128, 32).astype(np.uint8)
+    got = run(np.full(64, 127, np.uint8), np.concatenate([col, col]))
+    want = A.astype(np.float64) @ (B * np.exp2(col.astype(np.float64) - 127)[None, :])
+    bound = (np.abs(A) @ np.abs(B * np.exp2(col.astype(np.float64) - 127)[None, :])) * 64 * 2.0 ** -24
+    assert np.all(np.abs(got - want) <= bound)
+
+
+@pytest.mark.parametrize("kmax", [8, 40, 126])
+def test_scaled_cvt_per_element_power_of_two(probes, kmax):
+    """The dynamic P-scale casts P * 2^kj with kj up to 126 through the scaled
+    convert (scale 2^-kj, one per lane): bit-equal to the cast of the exact
+    product, for products in the range the rule produces (at most S = 2^8)."""
+    rng = np.random.default_rng(12 + kmax)
+    n = 1 << 20
+    k = rng.integers(0, kmax + 1, n // 2).repeat(2)
+    # P * 2^k in (0, 256]: P = 2^(u - k) with u in [-20, 8]
+    u = rng.uniform(-20, 8, n)
+    P = np.exp2(u - k).astype(np.float32)
+    P[::97] = np.float32(0.0)
+    scale = np.exp2(-k.astype(np.float64)).astype(np.float32)
+    xt, st = torch.from_numpy(P).cuda(), torch.from_numpy(scale).cuda()
+    out = torch.empty(n, dtype=torch.uint8, device="cuda")
+    assert probes.probe_cvt_scaled_vec(xt.data_ptr(), st.data_ptr(), n, out.data_ptr(), _stream()) == 0
+    exact = (P.astype(np.float64) * np.exp2(k)).astype(np.float32)
+    assert np.all(exact.astype(np.float64) == P.astype(np.float64) * np.exp2(k))
+    assert np.array_equal(out.cpu().numpy(), oracle.e4m3_encode(exact))
