@@ -228,12 +228,18 @@ def main() -> int:
     }
 
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(inp, w, order, S, out, cnt_np, sample_rows)
+        # the same workload with the dynamic per-block scale (S = 2^k0), for its MSE
+        out_dyn = None
+        if float(np.log2(S)).is_integer() and 0 <= np.log2(S) <= 8:
+            out_dyn, _ = A.fwd(q, k, v, S=S, order=order, causal=w.causal, block_kv=w.block_kv,
+                               mode=w.mode, want_lse=False, scale="dynamic")
+            torch.cuda.synchronize()
+        res["cpu_baseline"] = cpu_baseline(inp, w, order, S, out, cnt_np, sample_rows, out_dyn)
     print(json.dumps(res), flush=True)
     return 0
 
 
-def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows):
+def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows, out_dyn_dev=None):
     """The oracle (as it stands) on a bounded row sample of the same workload,
     plus P-cast MSE of the GPU output and of the oracle against FP64 attention."""
     import numpy as np
@@ -241,7 +247,8 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows):
     import oracle
 
     nthreads = min(16, oracle.default_threads())
-    every = max(1, (w.B * w.Hq * w.N) // 32768)
+    # about 10-15 s of oracle work on 16 host threads at the headline size
+    every = max(1, (w.B * w.Hq * w.N) // 524288)
     rows = np.arange(0, w.B * w.Hq * w.N, every, dtype=np.int64)
     rows = np.unique(np.concatenate([rows, sample_rows(w.B, w.Hq, w.N, 128, 10 ** 9, seed=0)[:64]]))
     keys = (rows % w.N + 1) if w.causal else np.full(rows.size, w.N)
@@ -255,6 +262,10 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows):
     g = out_dev.cpu().numpy().reshape(-1, w.d)[rows]
     mse_gpu = float(np.mean((g.astype(np.float64) - ref) ** 2))
     mse_oracle = float(np.mean((o_out.astype(np.float64) - ref) ** 2))
+    extra = {}
+    if out_dyn_dev is not None:
+        gd = out_dyn_dev.cpu().numpy().reshape(-1, w.d)[rows]
+        extra["mse_gpu_dynamic_scale_vs_fp64"] = float(np.mean((gd.astype(np.float64) - ref) ** 2))
     return {
         "value": round(flops / dt / 1e12, 6),
         "unit": "TFLOP/s",
@@ -267,6 +278,7 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows):
         "mse_oracle_vs_fp64": mse_oracle,
         "max_abs_gpu_minus_oracle": float(np.abs(g - o_out).max()),
         "counts_equal_on_sample": bool(np.array_equal(cnt_gpu[rows], o_cnt)),
+        **extra,
     }
 
 
