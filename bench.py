@@ -32,6 +32,10 @@ if ROOT not in sys.path:
 PEAK_TFLOPS = {"fp8": 5000.0, "bf16": 2500.0}
 # half of the FLOPs (QK^T) run on the bf16 MFMA, half (P.V) on the FP8 MFMA
 MIXED_PEAK = 2.0 / (1.0 / PEAK_TFLOPS["bf16"] + 1.0 / PEAK_TFLOPS["fp8"])
+# the arithmetic type of each mode's two contractions
+DTYPES = {"fast": "bf16 QK^T + e4m3 P.V, fp32 accumulate",
+          "fp8qk": "e4m3 QK^T + e4m3 P.V, fp32 accumulate",
+          "faithful": "fp32", "nocast": "fp32"}
 KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast.hip", "paper_2606_06521_amd/csrc/attn_common.hpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fast_kernel_causal_mha_b4_h32_n8192_d128.json")
 
@@ -140,6 +144,10 @@ def main() -> int:
         q = torch.from_numpy(inp.q_dev).cuda()
         k = torch.from_numpy(inp.k_dev).cuda()
         v = torch.from_numpy(inp.v_dev).cuda()
+    elif w.fmt == "e4m3":
+        q = torch.from_numpy(inp.q_dev).cuda().view(torch.float8_e4m3fn)
+        k = torch.from_numpy(inp.k_dev).cuda().view(torch.float8_e4m3fn)
+        v = torch.from_numpy(inp.v_dev).cuda().view(torch.float8_e4m3fn)
     else:
         q = torch.from_numpy(inp.q_dev.view(np.int16)).cuda().view(torch.bfloat16)
         k = torch.from_numpy(inp.k_dev.view(np.int16)).cuda().view(torch.bfloat16)
@@ -184,6 +192,9 @@ def main() -> int:
     kernel_ms = [s_ev.elapsed_time(e_ev) for s_ev, e_ev in ev]
     kernel_ms_avg = float(np.mean(kernel_ms))
     flops = w.flops()
+    # dense peak of the contraction dtype: FP8 MFMA for the fast modes (the
+    # spec denominator), FP32 matrix for the faithful ones
+    peak = PEAK_TFLOPS["fp8"] if w.mode in ("fast", "fp8qk") else 157.3
     value = flops / (ms_per_step * 1e-3) / 1e12
     achieved = flops / (kernel_ms_avg * 1e-3) / 1e12
 
@@ -205,7 +216,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16 QK^T + e4m3 P.V, fp32 accumulate" if w.mode == "fast" else "fp32",
+        "dtype": DTYPES[w.mode],
         "data": "synthetic (seeded sink workload, Delta=%g, 4 sink keys)" % delta,
         "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
                    "causal": w.causal, "mode": w.mode, "block_kv": w.block_kv, "order": order,
@@ -213,9 +224,9 @@ def main() -> int:
         "roofline": {
             "bound": "mfma",
             "achieved": round(achieved, 2),
-            "peak": PEAK_TFLOPS["fp8"] if w.mode == "fast" else 157.3,
+            "peak": peak,
             "unit": "TFLOP/s",
-            "frac": round(achieved / (PEAK_TFLOPS["fp8"] if w.mode == "fast" else 157.3), 4),
+            "frac": round(achieved / peak, 4),
             "traffic": measured_traffic(w.name),
             "kernel_ms_avg": round(kernel_ms_avg, 4),
             "flops_per_launch": flops,

@@ -42,6 +42,11 @@
  *                        instruction, E4M3 P bytes straight into the FP8 MFMA.
  *   ATTN_MODE_NOCAST   : like FAITHFUL with the cast disabled (P*S used as is);
  *                        a diagnostic for the FP64 comparison.
+ *   ATTN_MODE_FP8QK    : q, k and v all OCP E4M3 bytes.  Scores on the FP8 MFMA,
+ *                        the FP8 x FP8 -> FP32 scores of Algorithm 1; otherwise
+ *                        as FAST.  Per-tensor descales (Sec. 6.1: QKV
+ *                        quantization carries its own qscale/kscale/vscale) go
+ *                        through the *_descaled entry points.
  *   The E4M3 cast saturates: P*S >= 448 becomes 448 (reachable only for S > 448).
  *
  * Ownership and threading: every pointer is a device pointer owned by the
@@ -66,7 +71,8 @@ extern "C" {
 enum {
     ATTN_MODE_FAITHFUL = 0,
     ATTN_MODE_FAST = 1,
-    ATTN_MODE_NOCAST = 2
+    ATTN_MODE_NOCAST = 2,
+    ATTN_MODE_FP8QK = 3
 };
 
 /*
@@ -138,6 +144,31 @@ int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v,
                                int block_kv, int order, float S, int mode,
                                int n_sink, uint32_t* counts, float* out,
                                float* lse, void* stream);
+
+/*
+ * The two entry points above with per-tensor descales: the stored q, k, v
+ * values stand for q*q_descale, k*k_descale, v*v_descale (Sec. 6.1: the QKV
+ * quantization has its own scales, separate from the P-scale S).  With D the
+ * raw dot product of the stored q and k, the scores are
+ * z = D q_descale k_descale / sqrt(d): the device uses
+ * c = fl32(log2(e) q_descale k_descale / sqrt(d)) (rounded once from double)
+ * in place of log2(e)/sqrt(d), and the output is O / (S l) times v_descale.
+ * The plain entry points are these with all three descales 1.  Descales must
+ * be finite and > 0, else ATTN_ERR_INVALID_ARG.
+ */
+int attn_fp8_fwd_descaled(const void* q, const void* k, const void* v, float* out,
+                          float* lse, int B, int Hq, int Hkv, int N, int d,
+                          int causal, int block_kv, int order, float S, int mode,
+                          float q_descale, float k_descale, float v_descale,
+                          void* stream);
+
+int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void* v,
+                                        int B, int Hq, int Hkv, int N, int d,
+                                        int causal, int block_kv, int order, float S,
+                                        int mode, int n_sink, float q_descale,
+                                        float k_descale, float v_descale,
+                                        uint32_t* counts, float* out, float* lse,
+                                        void* stream);
 
 /* Static, human-readable text for a status code (never NULL). */
 const char* attn_fp8_strerror(int status);

@@ -54,8 +54,17 @@ def lib() -> ctypes.CDLL:
         L.oracle_e4m3_decode_array.restype = None
         L.oracle_attn.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, i32, P, i64, i32]
         L.oracle_attn.restype = i32
+        L.oracle_attn_descaled.argtypes = ([P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, i32]
+                                           + [f32, f32, f32, P, i64, i32])
+        L.oracle_attn_descaled.restype = i32
+        f64 = ctypes.c_double
+        L.oracle_attn_bound.argtypes = ([P] * 7 + [i32] * 8 + [f32, i32, i32, i32]
+                                        + [f32, f32, f32, f64, f64, P, i64, i32])
+        L.oracle_attn_bound.restype = i32
         L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
         L.oracle_ref_fp64.restype = i32
+        L.oracle_ref_fp64_descaled.argtypes = [P, P, P, P, P] + [i32] * 6 + [f64, f64, f64, P, i64, i32]
+        L.oracle_ref_fp64_descaled.restype = i32
         L.oracle_version.restype = i32
         _lib = L
     return _lib
@@ -91,14 +100,21 @@ def e4m3_decode(codes) -> np.ndarray:
 
 def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
          cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None,
-         scale: str = "static"):
+         scale: str = "static", descales=(1.0, 1.0, 1.0), bound_rel: float | None = None,
+         jitter_rel: float = 0.0):
     """Algorithm 1 on the given rows.
 
     q: [B,Hq,N,d]; k, v: [B,Hkv,N,d]; float32 arrays holding the exact values
     the device consumed.  rows: flat row ids ((b*Hq+hq)*N + r) or None for all.
     scale: "static" (one S for every block) or "dynamic" (per-block 2^kj from
     the block's P range, S = 2^k0 its floor; see oracle.c).
-    Returns (out [n_rows,d] float32, lse [n_rows] float32, counts [n_rows,3] uint32).
+    descales: per-tensor (q, k, v) descales of the stored values (Sec. 6.1).
+    bound_rel: if given, also return amb [n_rows,d], the bound on how far out
+    can move when every P*S within bound_rel (relative) of an E4M3 rounding
+    midpoint takes the other code (see oracle_attn_bound in oracle.c).
+    jitter_rel: planted exp2 error for the bound's own tests; 0 otherwise.
+    Returns (out [n_rows,d] float32, lse [n_rows] float32, counts [n_rows,3]
+    uint32[, amb [n_rows,d] float32]).
     """
     q = np.ascontiguousarray(q, dtype=np.float32)
     k = np.ascontiguousarray(k, dtype=np.float32)
@@ -114,16 +130,23 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     out = np.empty((n_rows, d), dtype=np.float32)
     lse = np.empty(n_rows, dtype=np.float32)
     counts = np.zeros((n_rows, 3), dtype=np.uint32)
-    rc = lib().oracle_attn(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
-                           B, Hq, Hkv, N, d, int(bool(causal)), int(block_kv),
-                           ORDER[order], float(S), int(bool(cast)), SCALE[scale], int(n_sink),
-                           _ptr(rows_a), n_rows, nthreads or default_threads())
+    amb = None if bound_rel is None else np.empty((n_rows, d), dtype=np.float32)
+    qd, kd, vd = (float(x) for x in descales)
+    rc = lib().oracle_attn_bound(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                                 _ptr(amb), B, Hq, Hkv, N, d, int(bool(causal)), int(block_kv),
+                                 ORDER[order], float(S), int(bool(cast)), SCALE[scale],
+                                 int(n_sink), qd, kd, vd, float(bound_rel or 0.0),
+                                 float(jitter_rel), _ptr(rows_a), n_rows,
+                                 nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_attn rejected its arguments")
+    if amb is not None:
+        return out, lse, counts, amb
     return out, lse, counts
 
 
-def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None = None):
+def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None = None,
+             descales=(1.0, 1.0, 1.0)):
     """Textbook softmax attention in FP64 (no blocks, no cast) on the given rows.
 
     Returns (out [n_rows,d] float64, lse [n_rows] float64).
@@ -141,9 +164,10 @@ def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None =
         n_rows = rows_a.size
     out = np.empty((n_rows, d), dtype=np.float64)
     lse = np.empty(n_rows, dtype=np.float64)
-    rc = lib().oracle_ref_fp64(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
-                               B, Hq, Hkv, N, d, int(bool(causal)),
-                               _ptr(rows_a), n_rows, nthreads or default_threads())
+    qd, kd, vd = (float(x) for x in descales)
+    rc = lib().oracle_ref_fp64_descaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                        B, Hq, Hkv, N, d, int(bool(causal)), qd, kd, vd,
+                                        _ptr(rows_a), n_rows, nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_ref_fp64 rejected its arguments")
     return out, lse

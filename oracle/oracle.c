@@ -49,7 +49,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORACLE_VERSION 2
+#define ORACLE_VERSION 4
 
 /* ------------------------------------------------------------------------- */
 /* OCP E4M3 (Sec. 2.1)                                                        */
@@ -148,6 +148,11 @@ typedef struct {
     int B, Hq, Hkv, N, d, causal, Bc, order, cast, n_sink;
     int scale_mode, k0;     /* k0 = log2 S (dynamic scale only) */
     float S;
+    double qk_descale;  /* q_descale * k_descale (exact in double) */
+    float v_descale;
+    float* amb;         /* [n_rows][d] code-ambiguity bound (nullable) */
+    double amb_rel;     /* relative half-width of the ambiguity window */
+    double jitter_rel;  /* planted exp2 error, test use only (0 = none) */
     const int64_t* rows;/* flat (b*Hq + hq)*N + r, n_rows of them */
     int64_t n_rows;
     int nthreads;
@@ -155,9 +160,18 @@ typedef struct {
     pthread_mutex_t lock;
 } attn_job;
 
+/* splitmix64 finaliser: a fixed hash of (row, key) for the planted jitter */
+static uint64_t mix64(uint64_t z)
+{
+    z += 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
 static void attn_row(const attn_job* J, int64_t flat, float* out_row,
-                     float* lse_row, uint32_t* cnt_row, float* D, float* P,
-                     float* o, float* blk)
+                     float* lse_row, uint32_t* cnt_row, float* amb_row, float* D,
+                     float* P, float* F, float* o, float* blk, float* a, float* ablk)
 {
     const int N = J->N, d = J->d, Bc = J->Bc;
     const int64_t bh = flat / N;
@@ -168,8 +182,10 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
     const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
     const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
     const float S = J->S;
-    /* exp(z) with z = D/sqrt(d) is exp2(D * c); c rounded once from double */
-    const float c = (float)(1.4426950408889634074 / sqrt((double)d));
+    /* exp(z) with z = D qd kd / sqrt(d) is exp2(D * c), D the raw dot of the
+     * stored values and qd, kd the per-tensor descales of the QKV
+     * quantization (Sec. 6.1); c rounded once from double */
+    const float c = (float)(1.4426950408889634074 * J->qk_descale / sqrt((double)d));
 
     const int L = J->causal ? r + 1 : N;        /* valid keys 0..L-1 */
     const int nblk = (L + Bc - 1) / Bc;
@@ -177,7 +193,7 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
     /* line: m <- -inf, l <- 0, O <- 0 (FP32) */
     float m = -INFINITY, mc = -INFINITY, ell = 0.0f;
     for (int i = 0; i < d; i++)
-        o[i] = 0.0f;
+        o[i] = a[i] = 0.0f;
     if (cnt_row)
         cnt_row[0] = cnt_row[1] = cnt_row[2] = 0;
 
@@ -208,7 +224,12 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         float psum = 0.0f;
         for (int t = 0; t < nt; t++) {
             const float x = fmaf(D[t], c, -mc_new);
-            P[t] = (float)exp2((double)x);
+            double e = exp2((double)x);
+            if (J->jitter_rel != 0.0) {
+                const uint64_t h = mix64(((uint64_t)flat << 32) ^ (uint64_t)(t0 + t));
+                e *= 1.0 + J->jitter_rel * (2.0 * ((double)(h >> 11) * 0x1p-53) - 1.0);
+            }
+            P[t] = (float)e;
             psum += P[t];
         }
         ell = alpha * ell + psum;
@@ -231,8 +252,16 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
          * zero codes per key category; the decoded value goes back to S units */
         for (int t = 0; t < nt; t++) {
             const float y = P[t] * Sj;
+            F[t] = 0.0f;
             if (J->cast == CAST_E4M3) {
                 const uint8_t e = oracle_e4m3_encode(y);
+                if (amb_row) {
+                    /* codes reachable from any y' within amb_rel of y: the
+                     * cast is monotone, so the two ends bound them */
+                    const uint8_t lo = oracle_e4m3_encode((float)((double)y * (1.0 - J->amb_rel)));
+                    const uint8_t hi = oracle_e4m3_encode((float)((double)y * (1.0 + J->amb_rel)));
+                    F[t] = ldexpf(oracle_e4m3_decode(hi) - oracle_e4m3_decode(lo), back);
+                }
                 if (cnt_row && e == 0x00) {
                     const int key = t0 + t;
                     const int cat = key < J->n_sink ? 0 : (key < Bc ? 1 : 2);
@@ -254,6 +283,18 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         }
         for (int i = 0; i < d; i++)
             o[i] = alpha * o[i] + blk[i];
+        if (amb_row) {
+            /* the same recurrence over |V| and the code spans */
+            for (int i = 0; i < d; i++)
+                ablk[i] = 0.0f;
+            for (int t = 0; t < nt; t++) {
+                const float* vt = V + (int64_t)(t0 + t) * d;
+                for (int i = 0; i < d; i++)
+                    ablk[i] += F[t] * fabsf(vt[i]);
+            }
+            for (int i = 0; i < d; i++)
+                a[i] = alpha * a[i] + ablk[i];
+        }
 
         m = m_new;
         mc = mc_new;
@@ -262,7 +303,10 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
     /* epilogue: O / (S * l); lse is the natural-log log-sum-exp of z */
     const float denom = S * ell;
     for (int i = 0; i < d; i++)
-        out_row[i] = o[i] / denom;
+        out_row[i] = o[i] / denom * J->v_descale;
+    if (amb_row)
+        for (int i = 0; i < d; i++)
+            amb_row[i] = a[i] / denom * J->v_descale;
     if (lse_row)
         *lse_row = (float)(((double)mc + log2((double)ell)) * 0.6931471805599453094);
 }
@@ -273,8 +317,11 @@ static void* attn_worker(void* arg)
     const int d = J->d, Bc = J->Bc;
     float* D = (float*)malloc(sizeof(float) * (size_t)Bc);
     float* P = (float*)malloc(sizeof(float) * (size_t)Bc);
+    float* F = (float*)malloc(sizeof(float) * (size_t)Bc);
     float* o = (float*)malloc(sizeof(float) * (size_t)d);
     float* blk = (float*)malloc(sizeof(float) * (size_t)d);
+    float* a = (float*)malloc(sizeof(float) * (size_t)d);
+    float* ablk = (float*)malloc(sizeof(float) * (size_t)d);
     for (;;) {
         int64_t i;
         pthread_mutex_lock(&J->lock);
@@ -284,12 +331,16 @@ static void* attn_worker(void* arg)
             break;
         const int64_t flat = J->rows ? J->rows[i] : i;
         attn_row(J, flat, J->out + i * (int64_t)d, J->lse ? J->lse + i : NULL,
-                 J->counts ? J->counts + 3 * i : NULL, D, P, o, blk);
+                 J->counts ? J->counts + 3 * i : NULL, J->amb ? J->amb + i * (int64_t)d : NULL,
+                 D, P, F, o, blk, a, ablk);
     }
     free(D);
     free(P);
+    free(F);
     free(o);
     free(blk);
+    free(a);
+    free(ablk);
     return NULL;
 }
 
@@ -326,18 +377,34 @@ static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
  *   cast: 0 = no cast (P*S used as is), 1 = E4M3.
  *   scale_mode: 0 = static S, 1 = dynamic per-block 2^kj (S must be 2^k0,
  *   0 <= k0 <= 8).
+ *   amb: [n_rows][d] (nullable), the code-ambiguity bound.  An implementation
+ *   whose exp2 is within a few ulps of the correctly rounded one may land a
+ *   P*S value that sits next to an E4M3 rounding midpoint on the other code.
+ *   amb[i] bounds what every such choice can move out[i]: with y = P*S and
+ *   F = decode(cast(y (1 + amb_rel))) - decode(cast(y (1 - amb_rel))) (zero
+ *   unless y lies within amb_rel of a midpoint), it runs the same recurrence
+ *   as O over F |V| and takes the same epilogue.  Both ends come from the
+ *   cast above, which is monotone in y.
+ *   jitter_rel: test use only (planting an exp2 error to check amb against);
+ *   when nonzero each exp2 of a P value is multiplied by 1 + jitter_rel * u,
+ *   u in [-1, 1) a fixed hash of (row, key).  0 for the method itself.
  * Returns 0, or -1 on an invalid argument.
  */
-int oracle_attn(const float* q, const float* k, const float* v, float* out,
-                float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
-                int d, int causal, int block_kv, int order, float S, int cast,
-                int scale_mode, int n_sink, const int64_t* rows, int64_t n_rows,
-                int nthreads)
+int oracle_attn_bound(const float* q, const float* k, const float* v, float* out,
+                      float* lse, uint32_t* counts, float* amb, int B, int Hq, int Hkv,
+                      int N, int d, int causal, int block_kv, int order, float S, int cast,
+                      int scale_mode, int n_sink, float q_descale, float k_descale,
+                      float v_descale, double amb_rel, double jitter_rel,
+                      const int64_t* rows, int64_t n_rows, int nthreads)
 {
+    if (!(amb_rel >= 0.0) || !(amb_rel < 0.5) || !(fabs(jitter_rel) < 0.5))
+        return -1;
     if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
         d < 1 || Hq % Hkv != 0 || block_kv < 1 || !(S > 0.0f) ||
         !isfinite(S) || (order != 0 && order != 1) || (cast != 0 && cast != 1) ||
-        (scale_mode != 0 && scale_mode != 1) || n_sink < 0 || n_rows < 0)
+        (scale_mode != 0 && scale_mode != 1) || n_sink < 0 || n_rows < 0 ||
+        !(q_descale > 0.0f) || !(k_descale > 0.0f) || !(v_descale > 0.0f) ||
+        !isfinite(q_descale) || !isfinite(k_descale) || !isfinite(v_descale))
         return -1;
     int k0 = 0;
     if (scale_mode == SCALE_DYNAMIC) {
@@ -360,8 +427,36 @@ int oracle_attn(const float* q, const float* k, const float* v, float* out,
     J.Bc = block_kv; J.order = order; J.cast = cast; J.n_sink = n_sink;
     J.scale_mode = scale_mode; J.k0 = k0;
     J.S = S; J.rows = rows; J.n_rows = n_rows; J.nthreads = nthreads;
+    J.qk_descale = (double)q_descale * (double)k_descale;
+    J.v_descale = v_descale;
+    J.amb = amb;
+    J.amb_rel = amb_rel;
+    J.jitter_rel = jitter_rel;
     run_threads(attn_worker, &J, &J.lock, nthreads);
     return 0;
+}
+
+int oracle_attn_descaled(const float* q, const float* k, const float* v, float* out,
+                         float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
+                         int d, int causal, int block_kv, int order, float S, int cast,
+                         int scale_mode, int n_sink, float q_descale, float k_descale,
+                         float v_descale, const int64_t* rows, int64_t n_rows,
+                         int nthreads)
+{
+    return oracle_attn_bound(q, k, v, out, lse, counts, NULL, B, Hq, Hkv, N, d, causal,
+                             block_kv, order, S, cast, scale_mode, n_sink, q_descale,
+                             k_descale, v_descale, 0.0, 0.0, rows, n_rows, nthreads);
+}
+
+int oracle_attn(const float* q, const float* k, const float* v, float* out,
+                float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
+                int d, int causal, int block_kv, int order, float S, int cast,
+                int scale_mode, int n_sink, const int64_t* rows, int64_t n_rows,
+                int nthreads)
+{
+    return oracle_attn_descaled(q, k, v, out, lse, counts, B, Hq, Hkv, N, d, causal,
+                                block_kv, order, S, cast, scale_mode, n_sink, 1.0f, 1.0f,
+                                1.0f, rows, n_rows, nthreads);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -374,6 +469,7 @@ typedef struct {
     double* out;
     double* lse;
     int B, Hq, Hkv, N, d, causal;
+    double qk_descale, v_descale;
     const int64_t* rows;
     int64_t n_rows, next;
     pthread_mutex_t lock;
@@ -400,7 +496,7 @@ static void* ref_worker(void* arg)
         const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
         const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
         const int L = J->causal ? r + 1 : N;
-        const double scale = 1.0 / sqrt((double)d);
+        const double scale = J->qk_descale / sqrt((double)d);
         double zmax = -INFINITY;
         for (int t = 0; t < L; t++) {
             double acc = 0.0;
@@ -422,7 +518,7 @@ static void* ref_worker(void* arg)
             for (int c = 0; c < d; c++)
                 o[c] += z[t] * (double)V[(int64_t)t * d + c];
         for (int c = 0; c < d; c++)
-            o[c] /= ell;
+            o[c] = o[c] / ell * J->v_descale;
         if (J->lse)
             J->lse[i] = zmax + log(ell);
     }
@@ -430,10 +526,11 @@ static void* ref_worker(void* arg)
     return NULL;
 }
 
-int oracle_ref_fp64(const float* q, const float* k, const float* v,
-                    double* out, double* lse, int B, int Hq, int Hkv, int N,
-                    int d, int causal, const int64_t* rows, int64_t n_rows,
-                    int nthreads)
+int oracle_ref_fp64_descaled(const float* q, const float* k, const float* v,
+                             double* out, double* lse, int B, int Hq, int Hkv, int N,
+                             int d, int causal, double q_descale, double k_descale,
+                             double v_descale, const int64_t* rows, int64_t n_rows,
+                             int nthreads)
 {
     if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
         d < 1 || Hq % Hkv != 0 || n_rows < 0)
@@ -449,8 +546,19 @@ int oracle_ref_fp64(const float* q, const float* k, const float* v,
     J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse;
     J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
     J.rows = rows; J.n_rows = n_rows;
+    J.qk_descale = q_descale * k_descale;
+    J.v_descale = v_descale;
     run_threads(ref_worker, &J, &J.lock, nthreads);
     return 0;
+}
+
+int oracle_ref_fp64(const float* q, const float* k, const float* v,
+                    double* out, double* lse, int B, int Hq, int Hkv, int N,
+                    int d, int causal, const int64_t* rows, int64_t n_rows,
+                    int nthreads)
+{
+    return oracle_ref_fp64_descaled(q, k, v, out, lse, B, Hq, Hkv, N, d, causal, 1.0, 1.0,
+                                    1.0, rows, n_rows, nthreads);
 }
 
 int oracle_version(void) { return ORACLE_VERSION; }

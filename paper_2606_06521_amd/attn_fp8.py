@@ -1,6 +1,6 @@
 """Python binding of libattn_fp8.so (argument marshalling only).
 
-The four C entry points are exposed under their C names; ``fwd`` and
+The C entry points are exposed under their C names; ``fwd`` and
 ``p_underflow_count`` are thin conveniences that take torch tensors on the GPU,
 check their dtypes and shapes, allocate outputs with torch and pass the
 current torch stream.  Every step of the computation runs in the HIP kernels;
@@ -16,12 +16,13 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libattn_fp8.so")
 
-ATTN_MODE_FAITHFUL, ATTN_MODE_FAST, ATTN_MODE_NOCAST = 0, 1, 2
+ATTN_MODE_FAITHFUL, ATTN_MODE_FAST, ATTN_MODE_NOCAST, ATTN_MODE_FP8QK = 0, 1, 2, 3
 ATTN_ORDER_FORWARD, ATTN_ORDER_REVERSE = 0, 1
 ATTN_OK, ATTN_ERR_INVALID_ARG, ATTN_ERR_UNSUPPORTED, ATTN_ERR_HIP = 0, -1, -2, -3
 ATTN_SCALE_DYNAMIC = 0x100
 
-MODES = {"faithful": ATTN_MODE_FAITHFUL, "fast": ATTN_MODE_FAST, "nocast": ATTN_MODE_NOCAST}
+MODES = {"faithful": ATTN_MODE_FAITHFUL, "fast": ATTN_MODE_FAST, "nocast": ATTN_MODE_NOCAST,
+         "fp8qk": ATTN_MODE_FP8QK}
 ORDERS = {"forward": ATTN_ORDER_FORWARD, "reverse": ATTN_ORDER_REVERSE}
 SCALES = {"static": 0, "dynamic": ATTN_SCALE_DYNAMIC}
 
@@ -35,6 +36,11 @@ _lib.attn_fp8_fwd.argtypes = [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P]
 _lib.attn_fp8_fwd.restype = _I
 _lib.attn_fp8_p_underflow_count.argtypes = [_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _P, _P, _P, _P]
 _lib.attn_fp8_p_underflow_count.restype = _I
+_lib.attn_fp8_fwd_descaled.argtypes = [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _F, _F, _F, _P]
+_lib.attn_fp8_fwd_descaled.restype = _I
+_lib.attn_fp8_p_underflow_count_descaled.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I]
+                                                     + [_F, _F, _F, _P, _P, _P, _P])
+_lib.attn_fp8_p_underflow_count_descaled.restype = _I
 _lib.attn_fp8_strerror.argtypes = [_I]
 _lib.attn_fp8_strerror.restype = ctypes.c_char_p
 _lib.attn_fp8_version.argtypes = []
@@ -58,6 +64,22 @@ def attn_fp8_p_underflow_count(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, orde
                                n_sink, counts, out, lse, stream):
     return _lib.attn_fp8_p_underflow_count(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order,
                                            float(S), mode, n_sink, counts, out, lse, stream)
+
+
+def attn_fp8_fwd_descaled(q, k, v, out, lse, B, Hq, Hkv, N, d, causal, block_kv, order, S, mode,
+                          q_descale, k_descale, v_descale, stream):
+    return _lib.attn_fp8_fwd_descaled(q, k, v, out, lse, B, Hq, Hkv, N, d, causal, block_kv,
+                                      order, float(S), mode, float(q_descale), float(k_descale),
+                                      float(v_descale), stream)
+
+
+def attn_fp8_p_underflow_count_descaled(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+                                        mode, n_sink, q_descale, k_descale, v_descale, counts,
+                                        out, lse, stream):
+    return _lib.attn_fp8_p_underflow_count_descaled(q, k, v, B, Hq, Hkv, N, d, causal, block_kv,
+                                                    order, float(S), mode, n_sink,
+                                                    float(q_descale), float(k_descale),
+                                                    float(v_descale), counts, out, lse, stream)
 
 
 def attn_fp8_strerror(status: int) -> str:
@@ -86,6 +108,9 @@ def _check(q, k, v, mode):
     if mode == ATTN_MODE_FAST:
         if q.dtype not in _FAST_QK or k.dtype not in _FAST_QK or v.dtype not in _FAST_V:
             raise TypeError("fast mode takes bfloat16 q/k and float8_e4m3fn (or uint8) v")
+    elif mode == ATTN_MODE_FP8QK:
+        if q.dtype not in _FAST_V or k.dtype not in _FAST_V or v.dtype not in _FAST_V:
+            raise TypeError("fp8qk mode takes float8_e4m3fn (or uint8) q, k and v")
     elif q.dtype != torch.float32 or k.dtype != torch.float32 or v.dtype != torch.float32:
         raise TypeError("faithful / nocast modes take float32 q, k, v")
     return B, Hq, k.shape[1], N, d
@@ -102,18 +127,19 @@ def _stream(stream):
 
 def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
         block_kv: int = 128, mode: str = "fast", out=None, lse=None, want_lse: bool = True,
-        stream=None, scale: str = "static"):
+        stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
     """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None).
-    scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8)."""
+    scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8);
+    descales = per-tensor (q, k, v) descales of the stored values."""
     m = MODES[mode]
     B, Hq, Hkv, N, d = _check(q, k, v, m)
     if out is None:
         out = torch.empty((B, Hq, N, d), dtype=torch.float32, device=q.device)
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
-    st = attn_fp8_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N, d,
-                      int(bool(causal)), int(block_kv), ORDERS[order], S, m | SCALES[scale],
-                      _stream(stream))
+    st = attn_fp8_fwd_descaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N,
+                               d, int(bool(causal)), int(block_kv), ORDERS[order], S,
+                               m | SCALES[scale], *descales, _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return out, lse
@@ -121,16 +147,15 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
 
 def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
                       block_kv: int = 128, mode: str = "fast", n_sink: int = 4, out=None, lse=None,
-                      stream=None, scale: str = "static"):
+                      stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
     """P-underflow diagnostic; returns counts [B,Hq,N,3] uint32 (as int32 storage)."""
     m = MODES[mode]
     B, Hq, Hkv, N, d = _check(q, k, v, m)
     counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
-    st = attn_fp8_p_underflow_count(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d,
-                                    int(bool(causal)), int(block_kv), ORDERS[order], S,
-                                    m | SCALES[scale],
-                                    int(n_sink), _ptr(counts), _ptr(out), _ptr(lse),
-                                    _stream(stream))
+    st = attn_fp8_p_underflow_count_descaled(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d,
+                                             int(bool(causal)), int(block_kv), ORDERS[order], S,
+                                             m | SCALES[scale], int(n_sink), *descales,
+                                             _ptr(counts), _ptr(out), _ptr(lse), _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return counts

@@ -40,6 +40,7 @@ struct Params {
     float S;             // static P-scale (2^k0 with the dynamic scale)
     float inv_S;         // 1/S, used only when S is a power of two (exact)
     int k0;              // log2 S (dynamic scale only)
+    float v_descale;     // per-tensor V descale, applied in the epilogue
     float c;             // fl32(log2(e) / sqrt(d))
     int n_tiles;         // query tiles per (batch, head)
     int total_wg;        // B * Hq * n_tiles

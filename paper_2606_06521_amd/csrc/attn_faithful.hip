@@ -248,10 +248,10 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
 #pragma unroll
                 for (int r4 = 0; r4 < 4; ++r4) {
                     f32x4 v4;
-                    v4[0] = o[dt][4 * r4 + 0] / denom;
-                    v4[1] = o[dt][4 * r4 + 1] / denom;
-                    v4[2] = o[dt][4 * r4 + 2] / denom;
-                    v4[3] = o[dt][4 * r4 + 3] / denom;
+                    v4[0] = o[dt][4 * r4 + 0] / denom * p.v_descale;
+                    v4[1] = o[dt][4 * r4 + 1] / denom * p.v_descale;
+                    v4[2] = o[dt][4 * r4 + 2] / denom * p.v_descale;
+                    v4[3] = o[dt][4 * r4 + 3] / denom * p.v_descale;
                     *reinterpret_cast<f32x4*>(orow + 32 * dt + 8 * r4 + 4 * h) = v4;
                 }
         }

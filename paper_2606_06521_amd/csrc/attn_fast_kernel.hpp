@@ -1,0 +1,576 @@
+// The fast kernel (template): bfloat16 Q and K (QK8 = false) or OCP E4M3 Q
+// and K (QK8 = true), OCP E4M3 V; the E4M3 P bytes feed the FP8 MFMA.
+// Instantiated by attn_fast.hip (bf16 Q/K) and attn_fast_qk8.hip (E4M3 Q/K).
+//
+// Algorithm 1 per query row with the kernel semantics of Sec. 6.1, one KV block
+// of BC keys per iteration, in forward or reverse block order:
+//   S^T = K_j Q^T        v_mfma_f32_32x32x16_bf16 (bf16) or
+//                        v_mfma_f32_32x32x64_f8f6f4 (E4M3, the FP8 x FP8
+//                        scores of Algorithm 1), FP32 accumulate (raw dots)
+//   m, alpha, P, l       per-lane scalars (one query row per lane)
+//   P8 = E4M3(P * S)     v_cvt_pk_fp8_f32 (round to nearest even); for S = 2^k
+//                        the scaled convert v_cvt_scalef32_pk_fp8_f32 applies
+//                        the exact power-of-two scale inside the convert; the
+//                        dynamic per-block scale 2^kj rides on the same convert
+//                        (per-lane scale) and on the P.V MFMA's E8M0 B scale
+//   O^T += V_j^T P8^T    v_mfma_f32_32x32x64_f8f6f4 (E4M3 x E4M3), FP32 accumulate
+//   out = O / (S l)
+//
+// Schedule ("ping-pong"): 8 waves of 32 query rows; waves w and w+4 share a
+// SIMD.  Group 0 (waves 0-3) and group 1 (waves 4-7) alternate between an MFMA
+// phase (P.V of the previous block, then S^T of the current block) and a VALU
+// phase (max, exp2, l, cast, rescale of O), one phase apart, with a workgroup
+// barrier between phases.  On every SIMD one wave keeps the matrix core busy
+// while the other runs the softmax.
+//
+// Grid: persistent, one workgroup per CU; each takes tile pairs (t, T-1-t)
+// of the heads of its XCD (unit_range), which equalises the causal work per
+// CU.
+//
+// K_j and V_j go global -> LDS with no register staging
+// (global_load_lds_dwordx4, lane i -> LDS base + 16 i), double-buffered, issued
+// by group 0 at the start of its MFMA phase two phases before first use.
+// K rows are stored in the order the S^T MFMA reads them (a key permutation
+// inside each 32-key tile, see a_row_to_key); V stays key-major and is read
+// transposed by ds_read_b64_tr_b8, which hands each lane 8 consecutive keys of
+// its d column.  Rows are unpadded; the 16-byte chunks of a row are permuted by
+// an XOR with a function of the row (kswz / vswz) so that the 16-byte K reads
+// and the transposed V reads of a lane group fall in distinct banks.  With
+// that layout a loading lane's HBM offset is a per-lane constant plus a
+// per-block scalar, so issuing a load costs no vector instructions.
+#pragma once
+
+#include "attn_common.hpp"
+#include "attn_launch.hpp"
+
+#include <math.h>
+#include <type_traits>
+
+namespace attn {
+
+namespace {
+
+typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+
+// One 16-byte-per-lane direct load: lane i reads HBM bytes [base + voff, +16)
+// (base uniform, voff per lane) and writes LDS bytes [dst + 16 i, +16).
+// Issued as inline assembly so the compiler does not tie its completion to
+// the next barrier; the kernel waits for it explicitly (wait_loads) before
+// the barrier that publishes the stage.  M0 holds the wave's LDS base and is
+// used by nothing else in this kernel.
+__device__ inline void g2lds16(const uint8_t* base, uint32_t voff, const uint8_t* dst_wave_base)
+{
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)dst_wave_base;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(base)
+                 : "memory");
+}
+
+__device__ inline void wait_loads()
+{
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+__device__ inline i32x2 lds_read_tr8(const uint8_t* p)
+{
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) i32x2*)(p));
+}
+
+}  // namespace
+
+// SCALE: kScaleAny (static S, multiply and convert), kScalePow2 (static
+// S = 2^k, the scaled convert) or kScaleDynamic (per-block 2^kj, see softmax).
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8>
+__global__ void __launch_bounds__(512) fast_kernel(Params p)
+{
+    constexpr int NW = 8;
+    constexpr int BM = 32 * NW;
+    constexpr int KT = BC / 32;                 // 32-key S^T tiles per block
+    constexpr int DK = QK8 ? D / 64 : D / 16;   // S^T MFMA k-steps over d
+    constexpr int DT = D / 32;                  // 32-wide d tiles of O^T
+    constexpr int PVS = BC / 64;                // 64-key FP8 MFMA k-steps
+    constexpr int KROW = QK8 ? D : D * 2;       // bytes per Q / K row (HBM and LDS)
+    constexpr int VROW = D;                     // bytes per V row
+    constexpr int KCPR = KROW / 16;             // 16-byte chunks per row
+    constexpr int VCPR = VROW / 16;
+    constexpr int K_BYTES = BC * KROW;          // one K stage
+    constexpr int V_BYTES = BC * VROW;
+    constexpr int K_RPI = 1024 / KROW;          // rows written by one wave load instruction
+    constexpr int V_RPI = 1024 / VROW;
+    constexpr int K_NI = K_BYTES / 4096;        // load instructions per loading wave (4 waves)
+    constexpr int V_NI = V_BYTES / 4096;
+    static_assert(K_NI >= 1 && V_NI >= 1, "stage smaller than one round of loads");
+
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks0[K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks1[K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs0[V_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs1[V_BYTES];
+
+    // Chunk swizzles: LDS row r of a stage stores logical 16-byte chunk L at
+    // physical chunk L ^ swz(r).  kswz spreads the 16 rows read by a 16-lane
+    // group (one logical chunk) over the 16 bank slots of 256 bytes; vswz does
+    // the same for the 8 rows x 2 chunks read by a 32-lane transposed read.
+    // Both depend only on row bits below 5, so they are the same for every
+    // 32-row (K) or 8-row (V) translate of a row.
+    auto kswz = [](int r) __attribute__((always_inline)) { return (r / (256 / KROW)) & (KCPR - 1); };
+    auto vswz = [](int r) __attribute__((always_inline)) { return ((r / (256 / VROW)) & (VCPR / 2 - 1)) * 2; };
+    // LDS row of a K stage -> key offset in the block
+    auto krow_key = [](int r) __attribute__((always_inline)) { return 32 * (r >> 5) + a_row_to_key(r & 31); };
+
+    // ---- persistent loop over this workgroup's tile pairs (heavier tile first) ----
+    const UnitRange ur = unit_range(p);
+    const int T = p.n_tiles;
+    for (long long u = ur.begin + ur.first; u < ur.end; u += ur.stride) {
+    for (int half = 0; half < 2; ++half) {
+        const int bh = (int)(u / p.pairs);
+        const int pr = (int)(u - (long long)bh * p.pairs);
+        const int tile = half == 0 ? T - 1 - pr : pr;
+        if (half == 1 && tile == T - 1 - pr)
+            break;                                    // odd tile count: the middle tile is alone
+        const int N = p.N;
+        const int b = bh / p.Hq;
+        const int hq = bh - b * p.Hq;
+        const int hk = hq / (p.Hq / p.Hkv);
+        const int tid = threadIdx.x;
+        const int lane = tid & 63;
+        const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, scalar
+        const int grp = w >> 2;                                   // 0: waves 0-3, 1: waves 4-7
+        const int n = lane & 31;
+        const int h = lane >> 5;
+        const int row0 = tile * BM;
+        const int wrow0 = row0 + 32 * w;
+        const int row = wrow0 + n;
+
+        const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * N * KROW;
+        const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)N;
+        const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
+        const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * D;
+
+        const int last_row_wg = min(row0 + BM, N) - 1;
+        const int nb = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
+        const bool wave_on = wrow0 < N;
+        // every row of a wave lies in one BC-block of rows (BC is a multiple of 32)
+        const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nb;
+        auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
+        auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
+
+        // ---- direct global -> LDS loads of one K / V stage (waves 0-3) ----
+        // Load instruction i = wl + 4 it of a stage (wl = w & 3) writes LDS bytes
+        // [1024 i, +1024): lane l fills row 4 K_RPI it + rho, rho = wl K_RPI +
+        // l / KCPR, physical chunk l % KCPR, i.e. logical chunk
+        // (l % KCPR) ^ kswz(rho) of key krow_key(4 K_RPI it) + krow_key(rho)
+        // (4 K_RPI is a power of two >= 16, so the two key parts have disjoint
+        // bits and the swizzle does not depend on it).  V likewise with
+        // key = row.  Keys past the end of the sequence (only in a ragged last
+        // block) read row N-1: they are masked to P = 0 before they can contribute.
+        const int wl = w & 3;
+        int k_key_l, v_key_l;
+        uint32_t k_chunk_l, v_chunk_l;
+        {
+            const int rk = wl * K_RPI + lane / KCPR;
+            k_key_l = krow_key(rk);
+            k_chunk_l = (uint32_t)(((lane % KCPR) ^ kswz(rk)) * 16);
+            const int rv = wl * V_RPI + lane / VCPR;
+            v_key_l = rv;
+            v_chunk_l = (uint32_t)(((lane % VCPR) ^ vswz(rv)) * 16);
+        }
+        const uint32_t k_voff = (uint32_t)k_key_l * KROW + k_chunk_l;
+        const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
+        auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if (t0 + BC <= N) {
+#pragma unroll
+                for (int it = 0; it < K_NI; ++it)
+                    g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
+                            dst + (wl + 4 * it) * 1024);
+            } else {
+#pragma unroll
+                for (int it = 0; it < K_NI; ++it) {
+                    const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, N - 1);
+                    g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
+                }
+            }
+        };
+        auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if (t0 + BC <= N) {
+#pragma unroll
+                for (int it = 0; it < V_NI; ++it)
+                    g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
+            } else {
+#pragma unroll
+                for (int it = 0; it < V_NI; ++it) {
+                    const int key = min(t0 + 4 * V_RPI * it + v_key_l, N - 1);
+                    g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
+                }
+            }
+        };
+
+        // Q^T fragments (B operand): lane (n, h) holds Q[row][16 kk + 8 h .. +8]
+        // (bf16) or Q[row][64 kk + 32 h .. +32] (E4M3)
+        using QFrag = std::conditional_t<QK8, i32x8, bf16x8>;
+        constexpr int QSTEP = QK8 ? 64 : 32;    // bytes of a Q row per k-step
+        QFrag qf[DK];
+        if (row < N) {
+            const uint8_t* qr = Qg + (size_t)row * KROW;
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk)
+                qf[kk] = *reinterpret_cast<const QFrag*>(qr + QSTEP * kk + (QSTEP / 2) * h);
+        } else {
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk)
+                qf[kk] = QFrag{};
+        }
+
+        // per-lane LDS offsets.  S^T A operand of k-step kk, tile kt: LDS row
+        // 32 kt + n, logical chunk 2 kk + h, i.e. (k_lane ^ (kk << 5)) + kt 32 KROW.
+        // V^T operand of d-tile dt: rows (j16 >> 1) + 16 h + {0, 8, 32, 40} + 64 js,
+        // logical chunk 2 dt + (n >> 4), half j16 & 1, i.e. (v_lane ^ (dt << 5)) +
+        // row offset.  (The XOR only touches chunk bits; row offsets are
+        // multiples of 8 rows and leave both swizzles unchanged.)
+        // E4M3 K: lane (n, h) reads logical chunks 4 kk + 2 h and 4 kk + 2 h + 1.
+        const uint32_t k_lane = (uint32_t)(n * KROW + (((QK8 ? 2 * h : h) ^ kswz(n)) << 4));
+        const uint32_t k_lane1 = (uint32_t)(n * KROW + (((2 * h + 1) ^ kswz(n)) << 4));
+        const int j16 = n & 15;                                   // lane within its 16-lane group
+        const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
+                                           8 * (j16 & 1));
+
+        const float c = p.c;
+        const float S = p.S;
+        const float inv_S = p.inv_S;
+        float m_run = -INFINITY;
+        float mc_run = -INFINITY;
+        float ell = 0.f;
+        f32x16 o[DT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                o[dt][r] = 0.f;
+        f32x16 s[KT];                 // S^T of the block between its MFMA and VALU phases
+        uint32_t pk[KT][4] = {};      // E4M3 P bytes between the VALU and the next MFMA phase
+        // dynamic scale: E8M0 byte 127 + k0 - kj of each row's block, the P.V
+        // MFMA's B-operand scale, which takes the block back to S units
+        int pv_sb = 127;
+        uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
+
+        // ---- S^T = K_j Q^T (register r of tile kt: key t0 + 32 kt + 16 h + r) ----
+        // The K fragments of k-step kk+2 are requested before the MFMAs of step
+        // kk are issued (three rotating register sets), so LDS latency and the
+        // CU-wide LDS bandwidth (shared with three other waves in this phase)
+        // overlap the matrix core; sched_barrier keeps the compiler from sinking
+        // the reads back next to their uses.
+        auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
+            auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
+                if constexpr (QK8) {
+                    const i32x4 lo = *reinterpret_cast<const i32x4*>(kst + (k_lane ^ (uint32_t)(kk << 6)) + kt * 32 * KROW);
+                    const i32x4 hi = *reinterpret_cast<const i32x4*>(kst + (k_lane1 ^ (uint32_t)(kk << 6)) + kt * 32 * KROW);
+                    return i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                } else {
+                    return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
+                }
+            };
+            constexpr int PF = DK >= 3 ? 2 : DK - 1;    // prefetch distance in k-steps
+            QFrag a[PF + 1][KT];
+#pragma unroll
+            for (int kk = 0; kk < PF; ++kk)
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+                    a[kk][kt] = kfrag(kk, kt);
+#pragma unroll
+            for (int kk = 0; kk < DK; ++kk) {
+                if (kk + PF < DK) {
+#pragma unroll
+                    for (int kt = 0; kt < KT; ++kt)
+                        a[(kk + PF) % (PF + 1)][kt] = kfrag(kk + PF, kt);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt) {
+                    const f32x16 acc = kk == 0 ? f32x16{} : s[kt];
+                    if constexpr (QK8)
+                        s[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[kk % (PF + 1)][kt], qf[kk], acc,
+                                                                                0, 0, 0, 0, 0, 0);
+                    else
+                        s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk % (PF + 1)][kt], qf[kk], acc, 0, 0, 0);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // ---- O^T += V_j^T P8^T ----
+        // The V^T operands are read (transposed) two MFMAs ahead of their use.
+        auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
+            auto vload = [&](int i) __attribute__((always_inline)) {
+                const int js = i / DT, dt = i % DT;
+                const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
+                const i32x2 r0 = lds_read_tr8(va);
+                const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
+                const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
+                const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
+                return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+            };
+            constexpr int NM = PVS * DT;                 // FP8 MFMAs per block
+            constexpr int PF = NM >= 3 ? 2 : NM - 1;
+            i32x8 av[PF + 1];
+#pragma unroll
+            for (int i = 0; i < PF; ++i)
+                av[i] = vload(i);
+#pragma unroll
+            for (int i = 0; i < NM; ++i) {
+                const int js = i / DT, dt = i % DT;
+                if (i + PF < NM)
+                    av[(i + PF) % (PF + 1)] = vload(i + PF);
+                i32x8 bop;
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    bop[q4] = (int)pk[2 * js][q4];
+                    bop[4 + q4] = (int)pk[2 * js + 1][q4];
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                if constexpr (SCALE == kScaleDynamic)
+                    o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0,
+                                                                            127, 0, pv_sb);
+                else
+                    o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av[i % (PF + 1)], bop, o[dt], 0, 0, 0,
+                                                                            0, 0, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        };
+
+        // ---- running max, alpha, P, l (pre-cast), E4M3 cast, rescale of O ----
+        auto softmax = [&](int j) __attribute__((always_inline)) {
+            const int t0 = j * BC;
+            if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
+                // key t0 + 32 kt + 16 h + r is valid iff 32 kt + r <= lim; masked
+                // scores become -inf through a sign-mask bit select (no compares)
+                const int lim = (CAUSAL ? min(row, N - 1) : N - 1) - t0 - 16 * h;
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const uint32_t m = (uint32_t)((lim - (32 * kt + r)) >> 31);
+                        const float sv = s[kt][r];
+                        const uint32_t x = __float_as_uint(sv);
+                        s[kt][r] = __uint_as_float((x & ~m) | (0xFF800000u & m));
+                    }
+            }
+            // row maximum: one independent chain per 32-key tile, then the tiles,
+            // then the two lane halves (a maximum is exact in any order)
+            float mk[KT];
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                float a = s[kt][0];
+#pragma unroll
+                for (int r = 1; r < 16; ++r)
+                    a = fmax_f(a, s[kt][r]);
+                mk[kt] = a;
+            }
+            float mx = mk[0];
+#pragma unroll
+            for (int kt = 1; kt < KT; ++kt)
+                mx = fmax_f(mx, mk[kt]);
+            mx = halves_max(mx);
+            const float m_new = fmax_f(m_run, mx);
+            const float mc_new = m_new * c;
+            const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
+            const float nmc = -mc_new;
+            // Dynamic P-scale (Limitations and Future Work, read as: the
+            // block's largest P lands in (S/2, S]): kj = k0 + clamp(floor(-xmax),
+            // 0, 126 - k0), xmax = fma(block max, c, -mc).  The convert scales
+            // by 2^kj (scale operand 2^-kj) and P.V by 2^(k0 - kj).
+            float cvt_scale = inv_S;
+            if constexpr (SCALE == kScaleDynamic) {
+                const float xmax = __builtin_fmaf(mx, c, nmc);
+                const float f = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(-xmax), 0.f),
+                                                (float)(126 - p.k0));
+                const int kj = p.k0 + (int)f;
+                cvt_scale = __uint_as_float((uint32_t)(127 - kj) << 23);
+                pv_sb = 127 + p.k0 - kj;
+            }
+            // The rest is organised in stages so that no instruction waits on the
+            // result of the one just before it (this phase runs alone on its
+            // SIMD's vector ALU while the partner wave drives the matrix core):
+            // (1) x = fma(D, c, -mc) for all keys, in place;
+            // (2) P = exp2(x) for all keys, in place, interleaved with the rescale
+            //     of O (independent work for the vector ALU while exp2 is in flight);
+            // (3) l from the pre-cast P (one partial sum per tile), E4M3 cast.
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    s[kt][r] = __builtin_fmaf(s[kt][r], c, nmc);
+            __builtin_amdgcn_sched_barrier(0);
+            // rescale O before this block's P.V; skipped when no row of the wave
+            // moved its maximum (alpha is then exactly 1)
+            const bool rescale = __ballot(alpha != 1.0f) != 0;
+            if (rescale) {
+#pragma unroll
+                for (int t = 0; t < DT; ++t)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        o[t][r] *= alpha;
+            }
+            {
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+            float lpart[KT];
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                float l0 = s[kt][0] + s[kt][1], l1 = s[kt][2] + s[kt][3];
+#pragma unroll
+                for (int r = 4; r < 16; r += 4) {
+                    l0 += s[kt][r] + s[kt][r + 1];
+                    l1 += s[kt][r + 2] + s[kt][r + 3];
+                }
+                lpart[kt] = l0 + l1;
+            }
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+                for (int r4 = 0; r4 < 4; ++r4) {
+                    const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
+                    const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
+                    uint32_t word;
+                    // The first convert writes the low half of the word, the second
+                    // the high half; the stale bytes of the previous block that the
+                    // word starts from are all overwritten (no zeroing needed).
+                    if constexpr (SCALE != kScaleAny) {
+                        s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, cvt_scale, false);
+                        lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, cvt_scale, true);
+                        word = __builtin_bit_cast(uint32_t, lo);
+                    } else {
+                        const float y0 = __builtin_fminf(p0 * S, 448.f);
+                        const float y1 = __builtin_fminf(p1 * S, 448.f);
+                        const float y2 = __builtin_fminf(p2 * S, 448.f);
+                        const float y3 = __builtin_fminf(p3 * S, 448.f);
+                        int wv = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, (int)pk[kt][r4], false);
+                        wv = __builtin_amdgcn_cvt_pk_fp8_f32(y2, y3, wv, true);
+                        word = (uint32_t)wv;
+                    }
+                    pk[kt][r4] = word;
+                    if (COUNT) {
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
+                            const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < N &&
+                                           (!CAUSAL || key <= row);
+                            if (z) {
+                                if (j > 0) ++cnt2;
+                                else if (key < p.n_sink) ++cnt0;
+                                else ++cnt1;
+                            }
+                        }
+                    }
+                }
+            }
+            float lsum = lpart[0];
+#pragma unroll
+            for (int kt = 1; kt < KT; ++kt)
+                lsum += lpart[kt];
+            ell = alpha * ell + lsum;
+            m_run = m_new;
+            mc_run = mc_new;
+        };
+
+        // ---- prologue: K of the first block into stage 0 ----
+        if (grp == 0)
+            load_k(Ks0, jof(0));
+        // Q fragments and the first K stage are complete after this point; the
+        // compiler sees the wait (it tracks no outstanding loads in the loop)
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        // Both groups run the same program -- per block k an MFMA phase (P.V of
+        // block k-1, S^T of block k) and a VALU phase (softmax of block k), each
+        // closed by a workgroup barrier -- but group 1 first passes one extra
+        // barrier, so it runs one phase behind group 0: while one wave of a SIMD
+        // is in its MFMA phase the other is in its softmax phase.  Group 0 issues
+        // the loads of K_{k+1} and V_k at the start of its MFMA phase k; they are
+        // first read two phases later.  Stage parity is k % 2 (the loop is
+        // unrolled twice so every LDS access names its stage statically).
+        if (grp == 1)
+            __syncthreads();
+        auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
+            __attribute__((always_inline)) {
+            if (grp == 0) {
+                if (k + 1 < nb)
+                    load_k(k_nxt, jof(k + 1));
+                if (k < nb)
+                    load_v(v_cur, jof(k));
+            }
+            // the wave in its MFMA phase takes issue priority over its SIMD
+            // partner in the VALU phase, so the matrix core is fed first
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(1);
+            __builtin_amdgcn_sched_barrier(0);
+            if (valid(k - 1))
+                pv(v_prv);
+            if (valid(k))
+                qk(k_cur);
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_setprio(0);
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            if (valid(k))
+                softmax(jof(k));
+            // the stage loads issued in the MFMA phase must land before the
+            // barrier that hands them to the next MFMA phase
+            if (grp == 0)
+                wait_loads();
+            __syncthreads();
+        };
+        for (int k = 0; k <= nb; k += 2) {
+            iteration(k, Ks0, Ks1, Vs0, Vs1);
+            if (k + 1 <= nb)
+                iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
+        }
+        if (grp == 0)
+            __syncthreads();
+
+        if (!wave_on)
+            continue;
+        const float ell_row = ell + other_half(ell);
+        if (COUNT) {
+            cnt0 += other_half_u32(cnt0);
+            cnt1 += other_half_u32(cnt1);
+            cnt2 += other_half_u32(cnt2);
+        }
+        if (row < N) {
+            const size_t flat = (size_t)bh * N + row;
+            if (p.out) {
+                const float inv = p.v_descale / (S * ell_row);
+                float* orow = p.out + flat * D;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        f32x4 v4;
+                        v4[0] = o[dt][4 * r4 + 0] * inv;
+                        v4[1] = o[dt][4 * r4 + 1] * inv;
+                        v4[2] = o[dt][4 * r4 + 2] * inv;
+                        v4[3] = o[dt][4 * r4 + 3] * inv;
+                        *reinterpret_cast<f32x4*>(orow + 32 * dt + 8 * r4 + 4 * h) = v4;
+                    }
+            }
+            if (h == 0) {
+                if (p.lse)
+                    p.lse[flat] = (mc_run + log2f(ell_row)) * 0.69314718055994531f;
+                if (COUNT) {
+                    p.counts[3 * flat + 0] = cnt0;
+                    p.counts[3 * flat + 1] = cnt1;
+                    p.counts[3 * flat + 2] = cnt2;
+                }
+            }
+        }
+    }  // tile of the pair
+    }  // unit
+}
+
+}  // namespace attn

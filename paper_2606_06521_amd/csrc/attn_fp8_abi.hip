@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kVersion = 200;   // 0.2.0: dynamic per-block scale
+constexpr int kVersion = 300;   // 0.3.0: dynamic per-block scale, E4M3 Q/K mode, descales
 
 bool is_pow2_scale(float S)
 {
@@ -22,7 +22,8 @@ bool is_pow2_scale(float S)
 // Shared validation and dispatch of both entry points.
 int run(const void* q, const void* k, const void* v, float* out, float* lse,
         uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int d, int causal,
-        int block_kv, int order, float S, int mode_flags, int n_sink, void* stream)
+        int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
+        float k_descale, float v_descale, void* stream)
 {
     const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
     const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
@@ -32,7 +33,11 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     if (order != ATTN_ORDER_FORWARD && order != ATTN_ORDER_REVERSE)
         return ATTN_ERR_INVALID_ARG;
-    if (mode != ATTN_MODE_FAITHFUL && mode != ATTN_MODE_FAST && mode != ATTN_MODE_NOCAST)
+    if (mode != ATTN_MODE_FAITHFUL && mode != ATTN_MODE_FAST && mode != ATTN_MODE_NOCAST &&
+        mode != ATTN_MODE_FP8QK)
+        return ATTN_ERR_INVALID_ARG;
+    if (!(q_descale > 0.0f) || !isfinite(q_descale) || !(k_descale > 0.0f) || !isfinite(k_descale) ||
+        !(v_descale > 0.0f) || !isfinite(v_descale))
         return ATTN_ERR_INVALID_ARG;
     if (!(S > 0.0f) || !isfinite(S))
         return ATTN_ERR_INVALID_ARG;
@@ -61,8 +66,8 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     if (count ? !counts : !out)
         return ATTN_ERR_INVALID_ARG;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
-    const int bm = (mode == ATTN_MODE_FAST) ? attn::fast_rows_per_wg(d, block_kv)
-                                            : attn::faithful_rows_per_wg();
+    const bool fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
+    const int bm = fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
     const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;
     const int64_t total = (int64_t)B * Hq * n_tiles;
     if (total > (int64_t)1 << 30)
@@ -84,8 +89,10 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.S = S;
     p.inv_S = 1.0f / S;
     p.k0 = k0;
-    // exp(z) = exp2(D * c) with z = D / sqrt(d): c rounded once from double
-    p.c = (float)(1.4426950408889634074 / sqrt((double)d));
+    // exp(z) = exp2(D * c) with z = D qd kd / sqrt(d) (D the raw dot of the
+    // stored values, qd and kd the per-tensor descales): c rounded once from double
+    p.c = (float)(1.4426950408889634074 * (double)q_descale * (double)k_descale / sqrt((double)d));
+    p.v_descale = v_descale;
     p.n_tiles = (int)n_tiles;
     p.total_wg = (int)total;
     p.per_xcd = (int)((total + attn::kNumXcd - 1) / attn::kNumXcd);
@@ -94,7 +101,7 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
-    if (mode == ATTN_MODE_FAST) {
+    if (fast) {
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
         const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
@@ -108,7 +115,10 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
         const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
                                                                             : per_xcd_max;
-        e = attn::launch_fast(p, (int)(per_xcd * attn::kNumXcd), d, block_kv, causal != 0, count, scale, s);
+        const int grid = (int)(per_xcd * attn::kNumXcd);
+        e = mode == ATTN_MODE_FP8QK
+                ? attn::launch_fast_qk8(p, grid, d, block_kv, causal != 0, count, scale, s)
+                : attn::launch_fast(p, grid, d, block_kv, causal != 0, count, scale, s);
     } else {
         e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, dyn, s);
     }
@@ -124,7 +134,7 @@ int attn_fp8_fwd(const void* q, const void* k, const void* v, float* out, float*
                  int mode, void* stream)
 {
     return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, d, causal, block_kv, order, S,
-               mode, 0, stream);
+               mode, 0, 1.0f, 1.0f, 1.0f, stream);
 }
 
 int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v, int B, int Hq,
@@ -133,7 +143,26 @@ int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v, int 
                                float* lse, void* stream)
 {
     return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
-               mode, n_sink, stream);
+               mode, n_sink, 1.0f, 1.0f, 1.0f, stream);
+}
+
+int attn_fp8_fwd_descaled(const void* q, const void* k, const void* v, float* out, float* lse,
+                          int B, int Hq, int Hkv, int N, int d, int causal, int block_kv,
+                          int order, float S, int mode, float q_descale, float k_descale,
+                          float v_descale, void* stream)
+{
+    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+               mode, 0, q_descale, k_descale, v_descale, stream);
+}
+
+int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void* v, int B,
+                                        int Hq, int Hkv, int N, int d, int causal, int block_kv,
+                                        int order, float S, int mode, int n_sink,
+                                        float q_descale, float k_descale, float v_descale,
+                                        uint32_t* counts, float* out, float* lse, void* stream)
+{
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+               mode, n_sink, q_descale, k_descale, v_descale, stream);
 }
 
 const char* attn_fp8_strerror(int status)
@@ -144,7 +173,7 @@ const char* attn_fp8_strerror(int status)
     case ATTN_ERR_INVALID_ARG:
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
                "and positive, or order/mode/causal/n_sink out of range; the dynamic scale "
-               "needs S = 2^k with 0 <= k <= 8)";
+               "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive)";
     case ATTN_ERR_UNSUPPORTED:
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:

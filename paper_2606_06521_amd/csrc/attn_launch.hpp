@@ -13,6 +13,9 @@ int faithful_rows_per_wg();
 // grid: a multiple of 8 workgroups, at most one per CU (persistent kernel)
 hipError_t launch_fast(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
                        int scale /* kScale* */, hipStream_t stream);
+// the same kernel with E4M3 Q and K (S^T on the FP8 MFMA)
+hipError_t launch_fast_qk8(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
+                           int scale /* kScale* */, hipStream_t stream);
 int fast_rows_per_wg(int d, int block_kv);
 
 }  // namespace attn

@@ -22,6 +22,19 @@ others).  Recipe:
 * V: float32 N(0, 1) for the FP32 modes; for the fast mode N(0, 1) divided by
   its per-tensor max |V| and rounded to OCP E4M3 (torch's float8_e4m3fn
   conversion, round to nearest even), so |V| <= 1.
+* E4M3 Q/K (fmt "e4m3", the FP8 x FP8 scores of Algorithm 1): N(0, 1)
+  clipped to +-4 and rounded to E4M3, values below 2^-1 in magnitude snapped
+  to the 2^-4 grid instead (every value is then an E4M3 value and a multiple
+  of 2^-4).  Products are multiples of 2^-8 of magnitude <= 16, so dots over
+  d <= 128 terms stay below 2^11 and are exact in FP32 in any order.  They are
+  also exact on the FP8 matrix cores of gfx950, which add products in groups
+  of eight aligned to the group's largest product and drop the bits more than
+  13 places below it (measured; a product <= 16 keeps bits down to 2^-9).  The sink
+  offset travels in the last SINK_CH8 channels: Q = 4 there, K = the E4M3 grid
+  value u with 4 * SINK_CH8 * u ~ sqrt(d) (Delta [t < n_sink] + b_t) (the same
+  u in every one of them); those channels are 0 for the other keys' offset
+  part.  Non-sink logits then have variance (d - SINK_CH8)/d.  V as in the
+  fast mode.
 
 Seeds: numpy PCG64; head (b, h) of each tensor draws from its own stream
 seeded by SeedSequence([seed, tensor, b, h]) (q = 1, k = 2, v = 3; the per-key
@@ -38,6 +51,9 @@ import torch
 
 GRID = 2.0 ** -5
 CLIP = 8.0 - GRID
+GRID8 = 2.0 ** -4      # E4M3 Q/K: grid of the small values
+CLIP8 = 4.0
+SINK_CH8 = 10          # E4M3 Q/K: channels carrying the sink offset
 
 
 @dataclass
@@ -54,7 +70,7 @@ class AttnInputs:
     Hkv: int
     N: int
     d: int
-    fmt: str                    # "f32" or "bf16_e4m3"
+    fmt: str                    # "f32", "bf16_e4m3" or "e4m3"
     delta: float
     n_sink: int
     q32: np.ndarray
@@ -87,6 +103,15 @@ def _bf16_bits(x: np.ndarray) -> np.ndarray:
         raise AssertionError("value not exact in bfloat16")
     # little-endian: the high 16 bits of each float32 are the odd uint16 halves
     return np.ascontiguousarray(u.view(np.uint16)[..., 1::2])
+
+
+def _e4m3_grid_inplace(x: np.ndarray) -> None:
+    """E4M3 values that are multiples of 2^-4, |x| <= 4, in place (E4M3 steps
+    are 2^-4 or coarser from 2^-1 up, so only smaller values need the grid)."""
+    np.clip(x, -CLIP8, CLIP8, out=x)
+    small = np.abs(x) < np.float32(0.5)
+    t = torch.from_numpy(x).to(torch.float8_e4m3fn).float().numpy()
+    x[...] = np.where(small, np.rint(x * np.float32(1 / GRID8)) * np.float32(GRID8), t)
 
 
 def _e4m3_codes(x: np.ndarray) -> tuple[np.ndarray, np.ndarray]:
@@ -138,9 +163,13 @@ def sink_channel(N: int, d: int, delta: float, n_sink: int, bias: np.ndarray | N
 def make_inputs(B: int, Hq: int, Hkv: int, N: int, d: int, *, fmt: str, delta: float,
                 seed: int, n_sink: int = 4, bias_var: float = 0.0,
                 sink_channel_on: bool = True) -> AttnInputs:
-    """Draw one problem.  fmt: "f32" (faithful / nocast) or "bf16_e4m3" (fast)."""
-    if fmt not in ("f32", "bf16_e4m3"):
+    """Draw one problem.  fmt: "f32" (faithful / nocast), "bf16_e4m3" (fast) or
+    "e4m3" (E4M3 Q/K/V)."""
+    if fmt not in ("f32", "bf16_e4m3", "e4m3"):
         raise ValueError(fmt)
+    if fmt == "e4m3":
+        return _make_inputs_e4m3(B, Hq, Hkv, N, d, delta=delta, seed=seed, n_sink=n_sink,
+                                 bias_var=bias_var, sink_channel_on=sink_channel_on)
     q = _normal_heads(seed, 1, B, Hq, N, d)
     k = _normal_heads(seed, 2, B, Hkv, N, d)
     v = _normal_heads(seed, 3, B, Hkv, N, d)
@@ -175,11 +204,69 @@ def make_inputs(B: int, Hq: int, Hkv: int, N: int, d: int, *, fmt: str, delta: f
     return AttnInputs(B, Hq, Hkv, N, d, fmt, delta, n_sink, q, k, v, q, k, v, delta_eff, meta)
 
 
+def sink_channel8(N: int, d: int, delta: float, n_sink: int, bias: np.ndarray | None) -> np.ndarray:
+    """E4M3 Q/K: the value u of K in each of the SINK_CH8 sink channels (Q = 4 there)."""
+    off = np.zeros(N, dtype=np.float64)
+    off[:n_sink] = delta
+    if bias is not None:
+        off = off + bias
+    u = (np.sqrt(d) * off / (4.0 * SINK_CH8)).astype(np.float32)
+    _e4m3_grid_inplace(u)
+    return u
+
+
+def _make_inputs_e4m3(B, Hq, Hkv, N, d, *, delta, seed, n_sink, bias_var, sink_channel_on):
+    q = _normal_heads(seed, 1, B, Hq, N, d)
+    k = _normal_heads(seed, 2, B, Hkv, N, d)
+    v = _normal_heads(seed, 3, B, Hkv, N, d)
+    bias = None
+    if bias_var > 0:
+        rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 4])))
+        bias = rng.standard_normal((B, Hkv, N)) * np.sqrt(bias_var)
+    _parallel_heads(lambda b, h: _e4m3_grid_inplace(q[b, h]), B, Hq)
+    _parallel_heads(lambda b, h: _e4m3_grid_inplace(k[b, h]), B, Hkv)
+    delta_eff = float("nan")
+    nc = min(SINK_CH8, d)
+    if sink_channel_on and N > 0:
+        q[..., d - nc:] = 4.0
+        for b in range(B):
+            for h in range(Hkv):
+                k[b, h, :, d - nc:] = sink_channel8(N, d, delta, n_sink,
+                                                    None if bias is None else bias[b, h])[:, None]
+        u0 = sink_channel8(max(n_sink, 1), d, delta, n_sink, None)[0]
+        delta_eff = float(4.0 * nc * u0 / np.sqrt(d))
+    amax = float(max(v.max(), -v.min())) if v.size else 1.0
+    v_codes = np.empty(v.shape, dtype=np.uint8)
+    q_codes = np.empty(q.shape, dtype=np.uint8)
+    k_codes = np.empty(k.shape, dtype=np.uint8)
+
+    def enc_v(b, h):
+        v[b, h] /= np.float32(amax)
+        v_codes[b, h], v[b, h] = _e4m3_codes(v[b, h])
+
+    def enc_q(b, h):
+        q_codes[b, h], dec = _e4m3_codes(q[b, h])
+        assert np.array_equal(dec, q[b, h])
+
+    def enc_k(b, h):
+        k_codes[b, h], dec = _e4m3_codes(k[b, h])
+        assert np.array_equal(dec, k[b, h])
+
+    _parallel_heads(enc_v, B, Hkv)
+    _parallel_heads(enc_q, B, Hq)
+    _parallel_heads(enc_k, B, Hkv)
+    meta = {"seed": seed, "bias_var": bias_var, "v_amax": amax}
+    return AttnInputs(B, Hq, Hkv, N, d, "e4m3", delta, n_sink, q, k, v, q_codes, k_codes,
+                      v_codes, delta_eff, meta)
+
+
 def with_delta(inp: AttnInputs, delta: float) -> AttnInputs:
     """Same base Q/K/V with only the sink keys' channel rewritten for a new Delta
     (paired runs, as in the paper's paired comparisons).  Requires bias_var == 0."""
     if inp.meta.get("bias_var", 0.0) > 0:
         raise ValueError("with_delta needs inputs without a per-key bias")
+    if inp.fmt == "e4m3":
+        raise ValueError("with_delta covers the f32 and bf16 formats")
     bf16 = inp.fmt == "bf16_e4m3"
     k32 = inp.k32.copy()
     ns = min(inp.n_sink, inp.N)

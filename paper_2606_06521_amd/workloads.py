@@ -27,6 +27,8 @@ class Workload:
 
     @property
     def fmt(self) -> str:
+        if self.mode == "fp8qk":
+            return "e4m3"
         return "f32" if self.mode in ("faithful", "nocast") else "bf16_e4m3"
 
     def flops(self) -> float:
@@ -47,6 +49,9 @@ WORKLOADS = {
         # causal MHA prefill, bf16 Q/K, e4m3 V, Delta = 7, reverse, S = 256
         Workload("causal_mha_b4_h32_n8192_d128_fast", 4, 32, 32, 8192, 128, True, "fast", 128,
                  (7.0,), (256.0,), ("reverse",), seed_base=20260300),
+        # the same with E4M3 Q and K (S^T on the FP8 MFMA as well)
+        Workload("causal_mha_b4_h32_n8192_d128_fp8qk", 4, 32, 32, 8192, 128, True, "fp8qk", 128,
+                 (7.0,), (256.0,), ("reverse",), seed_base=20260310),
         # causal GQA 64/8 heads at 32k, Delta = 9, S in {1, 256}, both orders
         Workload("causal_gqa_h64kv8_n32768_d128_fast", 1, 64, 8, 32768, 128, True, "fast", 128,
                  (9.0,), (1.0, 256.0), ("forward", "reverse"), seed_base=20260400),

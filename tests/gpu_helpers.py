@@ -9,8 +9,14 @@ import torch
 
 import oracle
 
-TOL_OUT = {"faithful": 2e-3, "nocast": 2e-3, "fast": 2e-2}
+TOL_OUT = {"faithful": 2e-3, "nocast": 2e-3, "fast": 2e-2, "fp8qk": 2e-2}
 TOL_LSE = 1e-4
+# The fast kernels take exp2 from v_exp_f32 (within 2 ulp of exact, see
+# test_gpu_probes), the oracle from a correctly rounded double.  With the
+# roundings of P and of P*S on both sides a P*S value can differ by up to
+# 3.5 ulp, so where it lies within 6 ulp of an E4M3 rounding midpoint both
+# codes are valid; the oracle's amb bounds what those choices move.
+AMB_WINDOW = 6.0 * 2.0 ** -23
 
 
 def log(msg: str) -> None:
@@ -23,6 +29,10 @@ def to_device(inp):
         q = torch.from_numpy(inp.q_dev).cuda()
         k = torch.from_numpy(inp.k_dev).cuda()
         v = torch.from_numpy(inp.v_dev).cuda()
+    elif inp.fmt == "e4m3":
+        q = torch.from_numpy(inp.q_dev).cuda().view(torch.float8_e4m3fn)
+        k = torch.from_numpy(inp.k_dev).cuda().view(torch.float8_e4m3fn)
+        v = torch.from_numpy(inp.v_dev).cuda().view(torch.float8_e4m3fn)
     else:
         q = torch.from_numpy(inp.q_dev.view(np.int16)).cuda().view(torch.bfloat16)
         k = torch.from_numpy(inp.k_dev.view(np.int16)).cuda().view(torch.bfloat16)
@@ -30,15 +40,16 @@ def to_device(inp):
     return q, k, v
 
 
-def run_gpu(dev, mode, S, order, causal, block_kv, n_sink=4, counts=True, scale="static"):
+def run_gpu(dev, mode, S, order, causal, block_kv, n_sink=4, counts=True, scale="static",
+            descales=(1.0, 1.0, 1.0)):
     from paper_2606_06521_amd import attn_fp8 as A
     q, k, v = dev
     out, lse = A.fwd(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv, mode=mode,
-                     scale=scale)
+                     scale=scale, descales=descales)
     cnt = None
     if counts:
         cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv,
-                                  mode=mode, n_sink=n_sink, scale=scale)
+                                  mode=mode, n_sink=n_sink, scale=scale, descales=descales)
     torch.cuda.synchronize()
     res = (out.cpu().numpy(), lse.cpu().numpy(), None if cnt is None else cnt.cpu().numpy().view(np.uint32))
     return res
@@ -53,29 +64,39 @@ def counts_are_exact(mode, S) -> bool:
     block j's threshold is the integer x <= -(10 + kj)."""
     if mode == "faithful":
         return True
-    if mode == "fast":
+    if mode in ("fast", "fp8qk"):
         return float(np.log2(S)).is_integer()
     return False
 
 
 def compare(inp, gpu, mode, S, order, causal, block_kv, rows=None, n_sink=4, label="",
-            scale="static"):
+            scale="static", descales=(1.0, 1.0, 1.0)):
     """Oracle on `rows` (flat ids, None = all); asserts counts bit-exact (where
     claimed) and out / lse within tolerance.  Returns the measured differences."""
     out_g, lse_g, cnt_g = gpu
     d = inp.d
-    o_out, o_lse, o_cnt = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,
-                                      block_kv=block_kv, causal=causal, cast=(mode != "nocast"),
-                                      n_sink=n_sink, rows=rows, scale=scale)
+    hw_exp2 = mode in ("fast", "fp8qk")
+    o_out, o_lse, o_cnt, amb = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,
+                                           block_kv=block_kv, causal=causal,
+                                           cast=(mode != "nocast"), n_sink=n_sink, rows=rows,
+                                           scale=scale, descales=descales,
+                                           bound_rel=AMB_WINDOW if hw_exp2 else 0.0)
     g_out = out_g.reshape(-1, d)
     g_lse = lse_g.reshape(-1)
     if rows is not None:
         g_out, g_lse = g_out[rows], g_lse[rows]
-    err = float(np.abs(g_out - o_out).max()) if g_out.size else 0.0
+    diff = np.abs(g_out.astype(np.float64) - o_out)
+    err = float(diff.max()) if g_out.size else 0.0
     lerr = float(np.abs(g_lse - o_lse).max()) if g_lse.size else 0.0
-    res = {"max_abs_out": err, "max_abs_lse": lerr}
+    # elements past the plain tolerance that the code-ambiguity bound covers
+    over = diff > TOL_OUT[mode]
+    res = {"max_abs_out": err, "max_abs_lse": lerr, "n_ambiguous_over_tol": int(over.sum())}
     assert np.all(np.isfinite(g_out)), label
-    assert err <= TOL_OUT[mode], (label, err)
+    bad = diff > TOL_OUT[mode] + amb
+    assert not bad.any(), (label, err, float((diff - amb)[bad].max()) if bad.any() else 0.0)
+    if over.any():
+        log(f"  {label}: {int(over.sum())} outputs past {TOL_OUT[mode]} (max {err:.4g}), "
+            f"all within the code-ambiguity bound")
     assert lerr <= TOL_LSE, (label, lerr)
     if cnt_g is not None and counts_are_exact(mode, S):
         g_cnt = cnt_g.reshape(-1, 3)

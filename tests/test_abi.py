@@ -25,8 +25,8 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(A):
     names = declared_functions()
-    assert names == ["attn_fp8_fwd", "attn_fp8_p_underflow_count", "attn_fp8_strerror",
-                     "attn_fp8_version"]
+    assert names == ["attn_fp8_fwd", "attn_fp8_fwd_descaled", "attn_fp8_p_underflow_count",
+                     "attn_fp8_p_underflow_count_descaled", "attn_fp8_strerror", "attn_fp8_version"]
     lib = ctypes.CDLL(A.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -40,7 +40,8 @@ def test_version_and_strerror(A):
 
 def test_enum_values_match_header(A):
     text = open(HEADER).read()
-    for name in ["ATTN_MODE_FAITHFUL", "ATTN_MODE_FAST", "ATTN_MODE_NOCAST", "ATTN_ORDER_FORWARD",
+    for name in ["ATTN_MODE_FAITHFUL", "ATTN_MODE_FAST", "ATTN_MODE_NOCAST", "ATTN_MODE_FP8QK",
+                 "ATTN_ORDER_FORWARD",
                  "ATTN_ORDER_REVERSE", "ATTN_OK", "ATTN_ERR_INVALID_ARG", "ATTN_ERR_UNSUPPORTED",
                  "ATTN_ERR_HIP"]:
         m = re.search(name + r"\s*=\s*(-?\d+)", text)
@@ -64,7 +65,7 @@ def fwd(A, **kw):
 @pytest.mark.parametrize("kw,status", [
     (dict(q=None), -1), (dict(k=None), -1), (dict(v=None), -1), (dict(out=None), -1),
     (dict(Hkv=3), -1), (dict(Hq=0), -1), (dict(B=-1), -1), (dict(N=-5), -1),
-    (dict(causal=2), -1), (dict(order=2), -1), (dict(mode=3), -1), (dict(mode=-1), -1),
+    (dict(causal=2), -1), (dict(order=2), -1), (dict(mode=4), -1), (dict(mode=-1), -1),
     (dict(S=0.0), -1), (dict(S=-1.0), -1), (dict(S=float("inf")), -1), (dict(S=float("nan")), -1),
     (dict(d=96), -2), (dict(d=256), -2), (dict(block_kv=32), -2), (dict(block_kv=256), -2),
     (dict(d=0), -1),
@@ -101,3 +102,23 @@ def test_binding_checks_dtypes_before_calling(A):
     q = torch.zeros((1, 1, 4, 64), dtype=torch.float32)
     with pytest.raises(ValueError):
         A.fwd(q, q, q, mode="faithful")          # host tensors are refused
+
+
+def test_descaled_entry_points_validate_descales(A):
+    base = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, lse=None, B=1, Hq=2, Hkv=1, N=64, d=64,
+                causal=0, block_kv=64, order=0, S=1.0, mode=3)
+
+    def f(qd, kd, vd, **kw):
+        a = dict(base, **kw)
+        return A.attn_fp8_fwd_descaled(a["q"], a["k"], a["v"], a["out"], a["lse"], a["B"],
+                                       a["Hq"], a["Hkv"], a["N"], a["d"], a["causal"],
+                                       a["block_kv"], a["order"], a["S"], a["mode"], qd, kd, vd,
+                                       None)
+    for bad in (0.0, -1.0, float("inf"), float("nan")):
+        assert f(bad, 1.0, 1.0) == -1
+        assert f(1.0, bad, 1.0) == -1
+        assert f(1.0, 1.0, bad) == -1
+    assert f(1.0, 1.0, 1.0, N=0, q=None, k=None, v=None, out=None) == 0
+    cnt = A.attn_fp8_p_underflow_count_descaled(FAKE, FAKE, FAKE, 1, 2, 1, 64, 64, 0, 64, 0, 1.0, 3,
+                                                4, 1.0, -2.0, 1.0, FAKE, None, None, None)
+    assert cnt == -1

@@ -45,6 +45,22 @@ def test_small_fast(d, bkv, causal, order):
 
 
 @pytest.mark.parametrize("d,bkv,causal,order", SMALL)
+def test_small_fp8qk(d, bkv, causal, order):
+    # E4M3 Q/K/V (scores on the FP8 MFMA), static and dynamic scales, with and
+    # without per-tensor descales
+    inp = make_inputs(2, 4, 2, 333, d, fmt="e4m3", delta=8.0, seed=600 + d + bkv)
+    dev = to_device(inp)
+    for S, scale, ds in [(1.0, "static", (1.0, 1.0, 1.0)), (256.0, "static", (1.0, 1.0, 1.0)),
+                         (448.0, "static", (1.0, 1.0, 1.0)), (3.0, "static", (1.0, 1.0, 1.0)),
+                         (256.0, "static", (0.75, 1.5, 2.0)), (256.0, "dynamic", (1.0, 1.0, 1.0)),
+                         (16.0, "dynamic", (1.25, 0.5, 0.5))]:
+        label = f"fp8qk d={d} bkv={bkv} causal={causal} {order} S={S} {scale} descales={ds}"
+        log(label)
+        gpu = run_gpu(dev, "fp8qk", S, order, causal, bkv, scale=scale, descales=ds)
+        compare(inp, gpu, "fp8qk", S, order, causal, bkv, label=label, scale=scale, descales=ds)
+
+
+@pytest.mark.parametrize("d,bkv,causal,order", SMALL)
 def test_small_dynamic_scale(d, bkv, causal, order):
     # dynamic per-block 2^kj scale in both modes: counts exact, outputs to the mode's bar
     for mode, fmt in (("faithful", "f32"), ("fast", "bf16_e4m3")):
@@ -88,9 +104,9 @@ def test_dynamic_scale_rejects_non_power_of_two():
 
 
 @pytest.mark.parametrize("N", [1, 31, 32, 33, 64, 65, 129])
-@pytest.mark.parametrize("mode", ["faithful", "fast"])
+@pytest.mark.parametrize("mode", ["faithful", "fast", "fp8qk"])
 def test_edge_lengths(N, mode):
-    fmt = "f32" if mode == "faithful" else "bf16_e4m3"
+    fmt = {"faithful": "f32", "fast": "bf16_e4m3", "fp8qk": "e4m3"}[mode]
     inp = make_inputs(1, 2, 1, N, 128, fmt=fmt, delta=9.0, seed=300 + N)
     dev = to_device(inp)
     for causal, order in itertools.product([False, True], ["forward", "reverse"]):
@@ -166,6 +182,20 @@ def test_workload_causal_mha_n8192_fast_full_size():
     gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv)
     res = compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows, label=label)
     log(str(res))
+
+
+def test_workload_causal_mha_n8192_fp8qk_full_size():
+    w = WORKLOADS["causal_mha_b4_h32_n8192_d128_fp8qk"]
+    inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    dev = to_device(inp)
+    rows = sample_rows(w.B, w.Hq, w.N, 128, 8, seed=1, per_tile=2)
+    for scale in ("static", "dynamic"):
+        label = f"{w.name} S=256 reverse {scale} (rows {rows.size})"
+        log(label)
+        gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv, scale=scale)
+        res = compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows,
+                      label=label, scale=scale)
+        log(str(res))
 
 
 def _heads_rows(N, heads, tile, every, seed, Hq):

@@ -7,7 +7,12 @@ CPU oracle or exact host arithmetic:
 - the scaled convert with scale 2^-k equals the plain convert of x * 2^k;
 - v_exp_f32 is exact at integers and monotone around them, so for S = 2^k the
   zero-code decision is x <= -(10 + k) on both sides;
-- the MFMA operand / accumulator lane layouts the kernels assume.
+- the MFMA operand / accumulator lane layouts the kernels assume;
+- how the matrix cores add products: the FP8 MFMA sums groups of eight
+  consecutive products aligned to the group's largest one and drops what lies
+  more than 13 bits below it (toward zero); the bf16 MFMA keeps 23 bits below
+  its largest product.  On the seeded inputs both are exact, which is what
+  makes the scores identical to the oracle's exact dot products.
 """
 import numpy as np
 import pytest
@@ -199,3 +204,70 @@ def test_scaled_cvt_per_element_power_of_two(probes, kmax):
     exact = (P.astype(np.float64) * np.exp2(k)).astype(np.float32)
     assert np.all(exact.astype(np.float64) == P.astype(np.float64) * np.exp2(k))
     assert np.array_equal(out.cpu().numpy(), oracle.e4m3_encode(exact))
+
+
+def _fp8_dot(probes, A, B):
+    Ac = torch.from_numpy(np.ascontiguousarray(A, np.float32)).to(torch.float8_e4m3fn)
+    Bc = torch.from_numpy(np.ascontiguousarray(B, np.float32)).to(torch.float8_e4m3fn)
+    assert np.array_equal(Ac.float().numpy(), A) and np.array_equal(Bc.float().numpy(), B)
+    D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+    assert probes.probe_mfma(1, Ac.view(torch.uint8).cuda().data_ptr(),
+                             Bc.view(torch.uint8).cuda().data_ptr(), D.data_ptr(), _stream()) == 0
+    return D.cpu().numpy().astype(np.float64)
+
+
+def _bf16_dot(probes, A, B):
+    At = torch.from_numpy(np.ascontiguousarray(A, np.float32)).to(torch.bfloat16)
+    Bt = torch.from_numpy(np.ascontiguousarray(B, np.float32)).to(torch.bfloat16)
+    assert np.array_equal(At.float().numpy(), A) and np.array_equal(Bt.float().numpy(), B)
+    D = torch.zeros((32, 32), dtype=torch.float32, device="cuda")
+    assert probes.probe_mfma(0, At.cuda().data_ptr(), Bt.cuda().data_ptr(), D.data_ptr(),
+                             _stream()) == 0
+    return D.cpu().numpy().astype(np.float64)
+
+
+def _two_products(K, big, i, small):
+    """A, B (power-of-two entries, E4M3 and bf16 exact) whose dot in every
+    output is big (channel 0) + small (channel i)."""
+    A = np.zeros((32, K), np.float32)
+    B = np.zeros((K, 32), np.float32)
+    for ch, v in ((0, big), (i, small)):
+        e = int(np.log2(abs(v)))
+        ea = max(e // 2, -9)
+        A[:, ch] = np.sign(v) * 2.0 ** ea
+        B[ch, :] = 2.0 ** (e - ea)
+    return A, B
+
+
+@pytest.mark.parametrize("big_exp", [0, 4])
+def test_mfma_fp8_groups_of_eight_truncate_13_bits_below(probes, big_exp):
+    big = 2.0 ** big_exp
+    for i in range(1, 64):
+        for f, sign in ((13, 1.0), (14, 1.0), (14, -1.0)):
+            small = sign * 2.0 ** (big_exp - f)
+            got = _fp8_dot(probes, *_two_products(64, big, i, small))
+            kept = f <= 13 or i >= 8
+            want = big + small if kept else big
+            assert np.all(got == want), (big_exp, i, f, sign, got[0, 0])
+
+
+def test_mfma_bf16_keeps_23_bits_below(probes):
+    for i in (1, 8, 15):
+        assert np.all(_bf16_dot(probes, *_two_products(16, 1.0, i, 2.0 ** -23)) == 1.0 + 2.0 ** -23)
+        assert np.all(_bf16_dot(probes, *_two_products(16, 1.0, i, 2.0 ** -24)) == 1.0)
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_matrix_core_dots_exact_on_seeded_inputs(probes, d):
+    from paper_2606_06521_amd.inputs import make_inputs
+    for fmt, K, dot in (("e4m3", 64, _fp8_dot), ("bf16_e4m3", 16, _bf16_dot)):
+        inp = make_inputs(1, 1, 1, 96, d, fmt=fmt, delta=9.0, seed=40 + d)
+        q, k = inp.q32[0, 0], inp.k32[0, 0]
+        # keys 0..31 hold the sink offset (n_sink = 4) and the rest; every
+        # K-wide slice of the channels, including the sink channels at the end
+        for c0 in range(0, d, K):
+            for r0 in (0, 32, 64):
+                A = q[r0:r0 + 32, c0:c0 + K]
+                B = k[0:32, c0:c0 + K].T
+                got = dot(probes, A, B)
+                assert np.array_equal(got, A.astype(np.float64) @ B.astype(np.float64)), (fmt, c0, r0)
