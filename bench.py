@@ -36,8 +36,14 @@ MIXED_PEAK = 2.0 / (1.0 / PEAK_TFLOPS["bf16"] + 1.0 / PEAK_TFLOPS["fp8"])
 DTYPES = {"fast": "bf16 QK^T + e4m3 P.V, fp32 accumulate",
           "fp8qk": "e4m3 QK^T + e4m3 P.V, fp32 accumulate",
           "faithful": "fp32", "nocast": "fp32"}
-KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast.hip", "paper_2606_06521_amd/csrc/attn_common.hpp"]
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fast_kernel_causal_mha_b4_h32_n8192_d128.json")
+KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast_kernel.hpp",
+                  "paper_2606_06521_amd/csrc/attn_fast.hip",
+                  "paper_2606_06521_amd/csrc/attn_fast_qk8.hip",
+                  "paper_2606_06521_amd/csrc/attn_common.hpp"]
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"traffic_fast_kernel_{workload}.json")
 
 
 def kernel_source_hash() -> str:
@@ -52,7 +58,7 @@ def measured_traffic(workload: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary, only
     if it was taken on the current kernel source and this workload."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(traffic_file(workload)) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
@@ -86,8 +92,9 @@ def write_traffic(fetch_csv: str, write_csv: str, workload: str, copy_mib: int =
 
     def read(path):
         rows = list(csv.DictReader(open(path)))
+        # the timed launches: causal, no counts, static power-of-two scale
         kern = [float(r["Counter_Value"]) for r in rows if "fast_kernel" in r["Kernel_Name"]
-                and "true, false" in r["Kernel_Name"]]
+                and ", true, false, 1," in r["Kernel_Name"]]
         copy = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
         return sum(kern) / len(kern), copy
 
@@ -107,7 +114,7 @@ def write_traffic(fetch_csv: str, write_csv: str, workload: str, copy_mib: int =
         "hbm_write_bytes_per_launch": w_kib * 1024 * w_scale,
         "hbm_bytes_per_launch": f_kib * 1024 * f_scale + w_kib * 1024 * w_scale,
     }
-    with open(TRAFFIC_FILE, "w") as f:
+    with open(traffic_file(workload), "w") as f:
         json.dump(t, f, indent=1)
     return t
 
