@@ -170,6 +170,43 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
                                         uint32_t* counts, float* out, float* lse,
                                         void* stream);
 
+/*
+ * Per-block diagnostic: where each KV block sits below the running maximum,
+ * and how many of its P values the cast zeroes.  The paper's collapse
+ * analysis assumes one sink cluster at key 0 and notes that with sinks spread
+ * over the sequence the sink gap Delta is replaced by the gap of each block
+ * (Limitations and Future Work, "Multi-sink patterns"; Prop. 1 for the
+ * zero codes).  This call measures that gap per (row, block) on the device,
+ * in the same pass as attn_fp8_p_underflow_count_descaled (same arguments,
+ * same counts / out / lse), and adds two aggregates over the rows:
+ *
+ *   gap_hist  device uint32 [B][Hq][nblk][nbins], nblk = ceil(N / block_kv).
+ *             For every row and every block j the row visits, with mx the
+ *             block's largest raw score of the row, mc = fl(m_new c) and
+ *             m_new the running maximum after block j, the gap
+ *             g = -fma(mx, c, -mc) (log2 units: the block's largest P is
+ *             2^-g) falls in bin min(max(floor(g), 0), nbins - 1), and
+ *             gap_hist[b][h][j][bin] counts it.  A block holding the running
+ *             maximum lands in bin 0; with S = 2^k the whole block is cast
+ *             to zero exactly when g >= 10 + k.
+ *   blk_zero  device uint32 [B][Hq][nblk]: zero codes of block j summed over
+ *             the rows (valid keys only, same rule as counts).  Zero in
+ *             no-cast mode.
+ *   nbins     1 .. 64.
+ *
+ * Both arrays are cleared by the call on `stream` (by a kernel, no memset)
+ * and filled with device atomics; their contents do not depend on the order
+ * of those atomics.  Returns ATTN_ERR_INVALID_ARG if nbins is out of range or
+ * a non-empty problem comes with a NULL gap_hist, blk_zero or counts; other
+ * arguments and return codes as for attn_fp8_p_underflow_count_descaled.
+ */
+int attn_fp8_block_gap_diag(const void* q, const void* k, const void* v, int B, int Hq,
+                            int Hkv, int N, int d, int causal, int block_kv, int order,
+                            float S, int mode, int n_sink, float q_descale,
+                            float k_descale, float v_descale, int nbins,
+                            uint32_t* gap_hist, uint32_t* blk_zero, uint32_t* counts,
+                            float* out, float* lse, void* stream);
+
 /* Static, human-readable text for a status code (never NULL). */
 const char* attn_fp8_strerror(int status);
 

@@ -61,6 +61,9 @@ def lib() -> ctypes.CDLL:
         L.oracle_attn_bound.argtypes = ([P] * 7 + [i32] * 8 + [f32, i32, i32, i32]
                                         + [f32, f32, f32, f64, f64, P, i64, i32])
         L.oracle_attn_bound.restype = i32
+        L.oracle_attn_diag.argtypes = ([P] * 9 + [i32] + [i32] * 8 + [f32, i32, i32, i32]
+                                       + [f32, f32, f32, f64, f64, P, i64, i32])
+        L.oracle_attn_diag.restype = i32
         L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
         L.oracle_ref_fp64.restype = i32
         L.oracle_ref_fp64_descaled.argtypes = [P, P, P, P, P] + [i32] * 6 + [f64, f64, f64, P, i64, i32]
@@ -143,6 +146,41 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     if amb is not None:
         return out, lse, counts, amb
     return out, lse, counts
+
+
+def block_diag(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
+               cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None,
+               scale: str = "static", descales=(1.0, 1.0, 1.0), nbins: int = 32):
+    """Algorithm 1 with the per-block diagnostic (see oracle_attn_diag in
+    oracle.c), accumulated over the given rows.
+    Returns (out, lse, counts, gap_hist [B,Hq,nblk,nbins] uint32,
+    blk_zero [B,Hq,nblk] uint32)."""
+    q = np.ascontiguousarray(q, dtype=np.float32)
+    k = np.ascontiguousarray(k, dtype=np.float32)
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    B, Hq, N, d = q.shape
+    Hkv = k.shape[1]
+    if rows is None:
+        n_rows = B * Hq * N
+        rows_a = None
+    else:
+        rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
+        n_rows = rows_a.size
+    nblk = (N + block_kv - 1) // block_kv
+    out = np.empty((n_rows, d), dtype=np.float32)
+    lse = np.empty(n_rows, dtype=np.float32)
+    counts = np.zeros((n_rows, 3), dtype=np.uint32)
+    hist = np.empty((B, Hq, nblk, nbins), dtype=np.uint32)
+    bz = np.empty((B, Hq, nblk), dtype=np.uint32)
+    qd, kd, vd = (float(x) for x in descales)
+    rc = lib().oracle_attn_diag(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                                None, _ptr(hist), _ptr(bz), int(nbins), B, Hq, Hkv, N, d,
+                                int(bool(causal)), int(block_kv), ORDER[order], float(S),
+                                int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd, 0.0, 0.0,
+                                _ptr(rows_a), n_rows, nthreads or default_threads())
+    if rc != 0:
+        raise ValueError("oracle_attn_diag rejected its arguments")
+    return out, lse, counts, hist, bz
 
 
 def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None = None,

@@ -18,7 +18,9 @@
  *     FP32 P, O from the cast P, round-to-nearest E4M3 cast of P*S, epilogue
  *     O / (S * l).
  *   - Prop. 1 (P-underflow condition): a P value underflows when its code is
- *     zero; the diagnostic counts those codes per key category.
+ *     zero; the diagnostic counts those codes per key category, and per
+ *     block together with each block's gap below the running maximum
+ *     (Limitations and Future Work, "Multi-sink patterns").
  *   - Limitations and Future Work, "worst-case vs average-case": a dynamic
  *     per-block power-of-two scale, chosen from the block's P range (only
  *     sketched in the paper; the rule below is this oracle's reading).
@@ -49,7 +51,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORACLE_VERSION 4
+#define ORACLE_VERSION 5
 
 /* ------------------------------------------------------------------------- */
 /* OCP E4M3 (Sec. 2.1)                                                        */
@@ -153,6 +155,9 @@ typedef struct {
     float* amb;         /* [n_rows][d] code-ambiguity bound (nullable) */
     double amb_rel;     /* relative half-width of the ambiguity window */
     double jitter_rel;  /* planted exp2 error, test use only (0 = none) */
+    uint32_t* gap_hist; /* [B*Hq][nblk_all][nbins] (nullable) */
+    uint32_t* blk_zero; /* [B*Hq][nblk_all] (nullable with gap_hist) */
+    int nbins, nblk_all;
     const int64_t* rows;/* flat (b*Hq + hq)*N + r, n_rows of them */
     int64_t n_rows;
     int nthreads;
@@ -220,6 +225,15 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         const float mc_new = m_new * c;
         const float alpha = (float)exp2((double)(mc - mc_new));
 
+        /* per-block diagnostic: the gap g = -(block's largest exponent
+         * argument), so the block's largest P is 2^-g; binned by floor */
+        if (J->gap_hist) {
+            const double g = floor(-(double)fmaf(mloc, c, -mc_new));
+            const int bin = g <= 0.0 ? 0 : (g >= J->nbins - 1 ? J->nbins - 1 : (int)g);
+            __atomic_fetch_add(&J->gap_hist[((int64_t)bh * J->nblk_all + j) * J->nbins + bin],
+                               1u, __ATOMIC_RELAXED);
+        }
+
         /* P = exp(Z - m_new) in FP32, l <- alpha*l + sum(P) (pre-cast) */
         float psum = 0.0f;
         for (int t = 0; t < nt; t++) {
@@ -267,6 +281,9 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
                     const int cat = key < J->n_sink ? 0 : (key < Bc ? 1 : 2);
                     cnt_row[cat]++;
                 }
+                if (J->blk_zero && e == 0x00)
+                    __atomic_fetch_add(&J->blk_zero[(int64_t)bh * J->nblk_all + j], 1u,
+                                       __ATOMIC_RELAXED);
                 P[t] = ldexpf(oracle_e4m3_decode(e), back);
             } else {
                 P[t] = ldexpf(y, back);
@@ -388,16 +405,28 @@ static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
  *   jitter_rel: test use only (planting an exp2 error to check amb against);
  *   when nonzero each exp2 of a P value is multiplied by 1 + jitter_rel * u,
  *   u in [-1, 1) a fixed hash of (row, key).  0 for the method itself.
+ *   gap_hist, blk_zero, nbins: the per-block diagnostic (both nullable, both
+ *   or neither; 1 <= nbins <= 64), accumulated over the given rows and zeroed
+ *   here first.  gap_hist[bh][j][bin] counts the rows that visit block j
+ *   with bin = min(max(floor(g), 0), nbins - 1), g = -fma(block max, c, -mc)
+ *   (the row's block maximum of the raw dots, mc = fl(m_new c) after the
+ *   block), i.e. the block's largest P is 2^-g: the multi-sink form of the
+ *   sink gap (Limitations and Future Work, "Multi-sink patterns").
+ *   blk_zero[bh][j] counts block j's zero codes over the rows (Prop. 1).
+ *   Both are [B*Hq][ceil(N/block_kv)](...) with bh = b*Hq + hq.
  * Returns 0, or -1 on an invalid argument.
  */
-int oracle_attn_bound(const float* q, const float* k, const float* v, float* out,
-                      float* lse, uint32_t* counts, float* amb, int B, int Hq, int Hkv,
-                      int N, int d, int causal, int block_kv, int order, float S, int cast,
-                      int scale_mode, int n_sink, float q_descale, float k_descale,
-                      float v_descale, double amb_rel, double jitter_rel,
-                      const int64_t* rows, int64_t n_rows, int nthreads)
+int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
+                     float* lse, uint32_t* counts, float* amb, uint32_t* gap_hist,
+                     uint32_t* blk_zero, int nbins, int B, int Hq, int Hkv, int N, int d,
+                     int causal, int block_kv, int order, float S, int cast, int scale_mode,
+                     int n_sink, float q_descale, float k_descale, float v_descale,
+                     double amb_rel, double jitter_rel, const int64_t* rows, int64_t n_rows,
+                     int nthreads)
 {
     if (!(amb_rel >= 0.0) || !(amb_rel < 0.5) || !(fabs(jitter_rel) < 0.5))
+        return -1;
+    if ((gap_hist != NULL) != (blk_zero != NULL) || (gap_hist && (nbins < 1 || nbins > 64)))
         return -1;
     if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
         d < 1 || Hq % Hkv != 0 || block_kv < 1 || !(S > 0.0f) ||
@@ -432,8 +461,28 @@ int oracle_attn_bound(const float* q, const float* k, const float* v, float* out
     J.amb = amb;
     J.amb_rel = amb_rel;
     J.jitter_rel = jitter_rel;
+    J.gap_hist = gap_hist;
+    J.blk_zero = blk_zero;
+    J.nbins = nbins;
+    J.nblk_all = (N + block_kv - 1) / block_kv;
+    if (gap_hist) {
+        memset(gap_hist, 0, sizeof(uint32_t) * (size_t)B * Hq * J.nblk_all * nbins);
+        memset(blk_zero, 0, sizeof(uint32_t) * (size_t)B * Hq * J.nblk_all);
+    }
     run_threads(attn_worker, &J, &J.lock, nthreads);
     return 0;
+}
+
+int oracle_attn_bound(const float* q, const float* k, const float* v, float* out,
+                      float* lse, uint32_t* counts, float* amb, int B, int Hq, int Hkv,
+                      int N, int d, int causal, int block_kv, int order, float S, int cast,
+                      int scale_mode, int n_sink, float q_descale, float k_descale,
+                      float v_descale, double amb_rel, double jitter_rel,
+                      const int64_t* rows, int64_t n_rows, int nthreads)
+{
+    return oracle_attn_diag(q, k, v, out, lse, counts, amb, NULL, NULL, 0, B, Hq, Hkv, N, d,
+                            causal, block_kv, order, S, cast, scale_mode, n_sink, q_descale,
+                            k_descale, v_descale, amb_rel, jitter_rel, rows, n_rows, nthreads);
 }
 
 int oracle_attn_descaled(const float* q, const float* k, const float* v, float* out,

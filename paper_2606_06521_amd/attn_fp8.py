@@ -41,6 +41,9 @@ _lib.attn_fp8_fwd_descaled.restype = _I
 _lib.attn_fp8_p_underflow_count_descaled.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I]
                                                      + [_F, _F, _F, _P, _P, _P, _P])
 _lib.attn_fp8_p_underflow_count_descaled.restype = _I
+_lib.attn_fp8_block_gap_diag.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _F, _F, _F, _I]
+                                         + [_P] * 5 + [_P])
+_lib.attn_fp8_block_gap_diag.restype = _I
 _lib.attn_fp8_strerror.argtypes = [_I]
 _lib.attn_fp8_strerror.restype = ctypes.c_char_p
 _lib.attn_fp8_version.argtypes = []
@@ -80,6 +83,15 @@ def attn_fp8_p_underflow_count_descaled(q, k, v, B, Hq, Hkv, N, d, causal, block
                                                     order, float(S), mode, n_sink,
                                                     float(q_descale), float(k_descale),
                                                     float(v_descale), counts, out, lse, stream)
+
+
+def attn_fp8_block_gap_diag(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order, S, mode, n_sink,
+                            q_descale, k_descale, v_descale, nbins, gap_hist, blk_zero, counts,
+                            out, lse, stream):
+    return _lib.attn_fp8_block_gap_diag(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order,
+                                        float(S), mode, n_sink, float(q_descale),
+                                        float(k_descale), float(v_descale), nbins, gap_hist,
+                                        blk_zero, counts, out, lse, stream)
 
 
 def attn_fp8_strerror(status: int) -> str:
@@ -159,3 +171,23 @@ def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", caus
     if st != ATTN_OK:
         raise AttnError(st)
     return counts
+
+
+def block_gap_diag(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
+                   block_kv: int = 128, mode: str = "fast", n_sink: int = 4, nbins: int = 32,
+                   stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
+    """Per-block diagnostic; returns (gap_hist [B,Hq,nblk,nbins], blk_zero [B,Hq,nblk],
+    counts [B,Hq,N,3]), all uint32 held in int32 storage."""
+    m = MODES[mode]
+    B, Hq, Hkv, N, d = _check(q, k, v, m)
+    nblk = (N + block_kv - 1) // block_kv
+    hist = torch.empty((B, Hq, nblk, nbins), dtype=torch.int32, device=q.device)
+    bz = torch.empty((B, Hq, nblk), dtype=torch.int32, device=q.device)
+    counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
+    st = attn_fp8_block_gap_diag(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(bool(causal)),
+                                 int(block_kv), ORDERS[order], S, m | SCALES[scale], int(n_sink),
+                                 *descales, int(nbins), _ptr(hist), _ptr(bz), _ptr(counts), None,
+                                 None, _stream(stream))
+    if st != ATTN_OK:
+        raise AttnError(st)
+    return hist, bz, counts

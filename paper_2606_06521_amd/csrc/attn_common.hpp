@@ -34,6 +34,14 @@ struct Params {
     float* out;
     float* lse;          // nullable
     uint32_t* counts;    // COUNT instantiations only
+    // per-block diagnostic (COUNT instantiations, both nullable):
+    // gap_hist[(bh * nblk_all + j) * nbins + bin] counts the rows whose gap
+    // g = -fma(block max, c, -mc) (log2 units) has min(max(floor(g), 0),
+    // nbins - 1) == bin; blk_zero[bh * nblk_all + j] counts block j's zero codes
+    uint32_t* gap_hist;
+    uint32_t* blk_zero;
+    int nbins;
+    int nblk_all;        // ceil(N / block_kv)
     int B, Hq, Hkv, N;
     int order;           // 0 forward, 1 reverse
     int n_sink;
@@ -123,6 +131,26 @@ __device__ inline float other_half(float x)
 __device__ inline uint32_t other_half_u32(uint32_t x)
 {
     return (uint32_t)__shfl_xor((int)x, 32, 64);
+}
+
+// Per-block diagnostic of one row: bin of the gap between the running maximum
+// and block j's largest score, g = -fma(block max, c, -mc) in log2 units (the
+// block's largest P is 2^-g), clamped to [0, nbins - 1]; one count per row.
+__device__ inline void record_gap(const Params& p, int bh, int j, float mx, float c, float nmc)
+{
+    const float g = __builtin_fmaxf(__builtin_floorf(-__builtin_fmaf(mx, c, nmc)), 0.f);
+    const int bin = (int)__builtin_fminf(g, (float)(p.nbins - 1));
+    atomicAdd(p.gap_hist + ((size_t)bh * p.nblk_all + j) * p.nbins + bin, 1u);
+}
+
+// Per-block diagnostic of one wave: adds the wave's zero codes of block j.
+__device__ inline void record_block_zeros(const Params& p, int bh, int j, uint32_t z)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1)
+        z += (uint32_t)__shfl_xor((int)z, off, 64);
+    if ((threadIdx.x & 63) == 0 && z != 0)
+        atomicAdd(p.blk_zero + (size_t)bh * p.nblk_all + j, z);
 }
 
 // max / sum of a value over the two 32-lane halves (lane i and lane i ^ 32),

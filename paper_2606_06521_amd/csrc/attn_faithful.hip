@@ -152,6 +152,8 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
         const float mc_new = m_new * c;
         const float alpha = (float)exp2((double)(mc_run - mc_new));
         const float nmc = -mc_new;
+        if (COUNT && p.gap_hist && h == 0 && row < N)
+            record_gap(p, bh, j, mx, c, nmc);
         // Dynamic P-scale: this block's rows cast P * 2^kj, kj = k0 +
         // clamp(floor(-xmax), 0, 126 - k0) with xmax = fma(block max, c, -mc),
         // and the decoded value goes back to S units times 2^(k0 - kj) (exact)
@@ -166,6 +168,7 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
 
         // ---- P = exp(Z - m_new); l from pre-cast P; P~ = E4M3(P*S) ----
         float lsum = 0.f;
+        uint32_t bz = 0;   // zero codes of this block (valid rows and keys)
         float pt[KT][16];
 #pragma unroll
         for (int kt = 0; kt < KT; ++kt) {
@@ -194,6 +197,8 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
                             if (z0) { if (k0 < p.n_sink) ++cnt0; else ++cnt1; }
                             if (z1) { if (k0 + 1 < p.n_sink) ++cnt0; else ++cnt1; }
                         }
+                        if (row < N)
+                            bz += z0 + z1;
                     }
                     const auto dec = __builtin_amdgcn_cvt_pk_f32_fp8(code, false);
                     y0 = dec[0];
@@ -208,6 +213,8 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
             }
         }
         ell = alpha * ell + lsum;
+        if (COUNT && CAST && p.blk_zero)
+            record_block_zeros(p, bh, j, bz);
 
         // ---- O <- alpha O + P~ V_j  (FP32 MFMA on O^T = V^T P~^T) ----
 #pragma unroll

@@ -376,6 +376,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             const float mc_new = m_new * c;
             const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
             const float nmc = -mc_new;
+            if (COUNT && p.gap_hist && h == 0 && row < N)
+                record_gap(p, bh, j, mx, c, nmc);
             // Dynamic P-scale (Limitations and Future Work, read as: the
             // block's largest P lands in (S/2, S]): kj = k0 + clamp(floor(-xmax),
             // 0, 126 - k0), xmax = fma(block max, c, -mc).  The convert scales
@@ -420,6 +422,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                         s[kt][r] = __builtin_amdgcn_exp2f(s[kt][r]);
             }
             __builtin_amdgcn_sched_barrier(0);
+            uint32_t bz = 0;   // zero codes of this block (valid rows and keys)
             float lpart[KT];
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
@@ -466,11 +469,14 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                                 if (j > 0) ++cnt2;
                                 else if (key < p.n_sink) ++cnt0;
                                 else ++cnt1;
+                                bz += row < N;
                             }
                         }
                     }
                 }
             }
+            if (COUNT && p.blk_zero)
+                record_block_zeros(p, bh, j, bz);
             float lsum = lpart[0];
 #pragma unroll
             for (int kt = 1; kt < KT; ++kt)

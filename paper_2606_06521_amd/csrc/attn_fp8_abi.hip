@@ -10,7 +10,16 @@
 
 namespace {
 
-constexpr int kVersion = 300;   // 0.3.0: dynamic per-block scale, E4M3 Q/K mode, descales
+constexpr int kVersion = 400;   // 0.4.0: per-block gap / zero-code diagnostic
+
+// Clears the diagnostic's output arrays on the caller's stream (a kernel, not
+// a memset node, so the call stays safe inside a captured graph).
+__global__ void zero_u32(uint32_t* a, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        a[i] = 0u;
+}
 
 bool is_pow2_scale(float S)
 {
@@ -23,7 +32,8 @@ bool is_pow2_scale(float S)
 int run(const void* q, const void* k, const void* v, float* out, float* lse,
         uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int d, int causal,
         int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
-        float k_descale, float v_descale, void* stream)
+        float k_descale, float v_descale, void* stream, uint32_t* gap_hist = nullptr,
+        uint32_t* blk_zero = nullptr, int nbins = 0)
 {
     const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
     const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
@@ -65,6 +75,8 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     if (count ? !counts : !out)
         return ATTN_ERR_INVALID_ARG;
+    if ((gap_hist || blk_zero) && (!count || !gap_hist || !blk_zero || nbins < 1 || nbins > 64))
+        return ATTN_ERR_INVALID_ARG;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
     const bool fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
     const int bm = fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
@@ -80,6 +92,10 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.out = out;
     p.lse = lse;
     p.counts = counts;
+    p.gap_hist = gap_hist;
+    p.blk_zero = blk_zero;
+    p.nbins = nbins;
+    p.nblk_all = (int)(((int64_t)N + block_kv - 1) / block_kv);
     p.B = B;
     p.Hq = Hq;
     p.Hkv = Hkv;
@@ -101,6 +117,13 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
 
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
+    if (gap_hist) {
+        const int64_t nz = (int64_t)B * Hq * p.nblk_all;
+        hipLaunchKernelGGL(zero_u32, dim3(1024), dim3(256), 0, s, gap_hist, nz * nbins);
+        hipLaunchKernelGGL(zero_u32, dim3(1024), dim3(256), 0, s, blk_zero, nz);
+        if (hipGetLastError() != hipSuccess)
+            return ATTN_ERR_HIP;
+    }
     if (fast) {
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
@@ -165,6 +188,20 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
                mode, n_sink, q_descale, k_descale, v_descale, stream);
 }
 
+int attn_fp8_block_gap_diag(const void* q, const void* k, const void* v, int B, int Hq, int Hkv,
+                            int N, int d, int causal, int block_kv, int order, float S, int mode,
+                            int n_sink, float q_descale, float k_descale, float v_descale,
+                            int nbins, uint32_t* gap_hist, uint32_t* blk_zero, uint32_t* counts,
+                            float* out, float* lse, void* stream)
+{
+    if (nbins < 1 || nbins > 64)
+        return ATTN_ERR_INVALID_ARG;
+    if (B > 0 && Hq > 0 && N > 0 && (!gap_hist || !blk_zero))
+        return ATTN_ERR_INVALID_ARG;
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+               mode, n_sink, q_descale, k_descale, v_descale, stream, gap_hist, blk_zero, nbins);
+}
+
 const char* attn_fp8_strerror(int status)
 {
     switch (status) {
@@ -173,7 +210,8 @@ const char* attn_fp8_strerror(int status)
     case ATTN_ERR_INVALID_ARG:
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
                "and positive, or order/mode/causal/n_sink out of range; the dynamic scale "
-               "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive)";
+               "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive; "
+               "the block diagnostic needs all three arrays and 1 <= nbins <= 64)";
     case ATTN_ERR_UNSUPPORTED:
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:

@@ -25,8 +25,9 @@ def declared_functions():
 
 def test_exports_every_declared_symbol(A):
     names = declared_functions()
-    assert names == ["attn_fp8_fwd", "attn_fp8_fwd_descaled", "attn_fp8_p_underflow_count",
-                     "attn_fp8_p_underflow_count_descaled", "attn_fp8_strerror", "attn_fp8_version"]
+    assert names == ["attn_fp8_block_gap_diag", "attn_fp8_fwd", "attn_fp8_fwd_descaled",
+                     "attn_fp8_p_underflow_count", "attn_fp8_p_underflow_count_descaled",
+                     "attn_fp8_strerror", "attn_fp8_version"]
     lib = ctypes.CDLL(A.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -122,3 +123,24 @@ def test_descaled_entry_points_validate_descales(A):
     cnt = A.attn_fp8_p_underflow_count_descaled(FAKE, FAKE, FAKE, 1, 2, 1, 64, 64, 0, 64, 0, 1.0, 3,
                                                 4, 1.0, -2.0, 1.0, FAKE, None, None, None)
     assert cnt == -1
+
+
+def test_block_gap_diag_validates_before_any_launch(A):
+    def g(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, B=1, Hq=2, Hkv=1, N=64, d=64, causal=0, block_kv=64,
+                 order=0, S=256.0, mode=1, n_sink=4, qd=1.0, kd=1.0, vd=1.0, nbins=16,
+                 hist=FAKE, bz=FAKE, counts=FAKE)
+        a.update(kw)
+        return A.attn_fp8_block_gap_diag(a["q"], a["k"], a["v"], a["B"], a["Hq"], a["Hkv"],
+                                         a["N"], a["d"], a["causal"], a["block_kv"], a["order"],
+                                         a["S"], a["mode"], a["n_sink"], a["qd"], a["kd"],
+                                         a["vd"], a["nbins"], a["hist"], a["bz"], a["counts"],
+                                         None, None, None)
+    for bad in (0, 65, -3):
+        assert g(nbins=bad) == -1
+    assert g(hist=None) == -1
+    assert g(bz=None) == -1
+    assert g(counts=None) == -1
+    assert g(qd=0.0) == -1
+    assert g(d=32) == -2
+    assert g(N=0, q=None, k=None, v=None, hist=None, bz=None, counts=None) == 0
