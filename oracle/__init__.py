@@ -64,6 +64,11 @@ def lib() -> ctypes.CDLL:
         L.oracle_attn_diag.argtypes = ([P] * 9 + [i32] + [i32] * 8 + [f32, i32, i32, i32]
                                        + [f32, f32, f32, f64, f64, P, i64, i32])
         L.oracle_attn_diag.restype = i32
+        L.oracle_attn_full.argtypes = ([P] * 9 + [i32] + [i32] * 9 + [f32, i32, i32, i32]
+                                       + [f32, f32, f32, f64, f64, P, i64, i32])
+        L.oracle_attn_full.restype = i32
+        L.oracle_ref_fp64_kv.argtypes = [P, P, P, P, P] + [i32] * 7 + [f64, f64, f64, P, i64, i32]
+        L.oracle_ref_fp64_kv.restype = i32
         L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
         L.oracle_ref_fp64.restype = i32
         L.oracle_ref_fp64_descaled.argtypes = [P, P, P, P, P] + [i32] * 6 + [f64, f64, f64, P, i64, i32]
@@ -107,8 +112,10 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
          jitter_rel: float = 0.0):
     """Algorithm 1 on the given rows.
 
-    q: [B,Hq,N,d]; k, v: [B,Hkv,N,d]; float32 arrays holding the exact values
-    the device consumed.  rows: flat row ids ((b*Hq+hq)*N + r) or None for all.
+    q: [B,Hq,Nq,d]; k, v: [B,Hkv,Nk,d] (Nq <= Nk; query row r sits at key
+    position Nk - Nq + r, so Nq = Nk is plain self-attention); float32 arrays
+    holding the exact values the device consumed.  rows: flat row ids
+    ((b*Hq+hq)*Nq + r) or None for all.
     scale: "static" (one S for every block) or "dynamic" (per-block 2^kj from
     the block's P range, S = 2^k0 its floor; see oracle.c).
     descales: per-tensor (q, k, v) descales of the stored values (Sec. 6.1).
@@ -122,10 +129,10 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     q = np.ascontiguousarray(q, dtype=np.float32)
     k = np.ascontiguousarray(k, dtype=np.float32)
     v = np.ascontiguousarray(v, dtype=np.float32)
-    B, Hq, N, d = q.shape
-    Hkv = k.shape[1]
+    B, Hq, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
     if rows is None:
-        n_rows = B * Hq * N
+        n_rows = B * Hq * Nq
         rows_a = None
     else:
         rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
@@ -135,12 +142,12 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     counts = np.zeros((n_rows, 3), dtype=np.uint32)
     amb = None if bound_rel is None else np.empty((n_rows, d), dtype=np.float32)
     qd, kd, vd = (float(x) for x in descales)
-    rc = lib().oracle_attn_bound(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
-                                 _ptr(amb), B, Hq, Hkv, N, d, int(bool(causal)), int(block_kv),
-                                 ORDER[order], float(S), int(bool(cast)), SCALE[scale],
-                                 int(n_sink), qd, kd, vd, float(bound_rel or 0.0),
-                                 float(jitter_rel), _ptr(rows_a), n_rows,
-                                 nthreads or default_threads())
+    rc = lib().oracle_attn_full(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                                _ptr(amb), None, None, 0, B, Hq, Hkv, Nq, Nk, d,
+                                int(bool(causal)), int(block_kv), ORDER[order], float(S),
+                                int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd,
+                                float(bound_rel or 0.0), float(jitter_rel), _ptr(rows_a), n_rows,
+                                nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_attn rejected its arguments")
     if amb is not None:
@@ -158,23 +165,23 @@ def block_diag(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = F
     q = np.ascontiguousarray(q, dtype=np.float32)
     k = np.ascontiguousarray(k, dtype=np.float32)
     v = np.ascontiguousarray(v, dtype=np.float32)
-    B, Hq, N, d = q.shape
-    Hkv = k.shape[1]
+    B, Hq, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
     if rows is None:
-        n_rows = B * Hq * N
+        n_rows = B * Hq * Nq
         rows_a = None
     else:
         rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
         n_rows = rows_a.size
-    nblk = (N + block_kv - 1) // block_kv
+    nblk = (Nk + block_kv - 1) // block_kv
     out = np.empty((n_rows, d), dtype=np.float32)
     lse = np.empty(n_rows, dtype=np.float32)
     counts = np.zeros((n_rows, 3), dtype=np.uint32)
     hist = np.empty((B, Hq, nblk, nbins), dtype=np.uint32)
     bz = np.empty((B, Hq, nblk), dtype=np.uint32)
     qd, kd, vd = (float(x) for x in descales)
-    rc = lib().oracle_attn_diag(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
-                                None, _ptr(hist), _ptr(bz), int(nbins), B, Hq, Hkv, N, d,
+    rc = lib().oracle_attn_full(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                                None, _ptr(hist), _ptr(bz), int(nbins), B, Hq, Hkv, Nq, Nk, d,
                                 int(bool(causal)), int(block_kv), ORDER[order], float(S),
                                 int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd, 0.0, 0.0,
                                 _ptr(rows_a), n_rows, nthreads or default_threads())
@@ -192,10 +199,10 @@ def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None =
     q = np.ascontiguousarray(q, dtype=np.float32)
     k = np.ascontiguousarray(k, dtype=np.float32)
     v = np.ascontiguousarray(v, dtype=np.float32)
-    B, Hq, N, d = q.shape
-    Hkv = k.shape[1]
+    B, Hq, Nq, d = q.shape
+    Hkv, Nk = k.shape[1], k.shape[2]
     if rows is None:
-        n_rows = B * Hq * N
+        n_rows = B * Hq * Nq
         rows_a = None
     else:
         rows_a = np.ascontiguousarray(np.asarray(rows, dtype=np.int64))
@@ -203,9 +210,9 @@ def ref_fp64(q, k, v, *, causal: bool = False, rows=None, nthreads: int | None =
     out = np.empty((n_rows, d), dtype=np.float64)
     lse = np.empty(n_rows, dtype=np.float64)
     qd, kd, vd = (float(x) for x in descales)
-    rc = lib().oracle_ref_fp64_descaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
-                                        B, Hq, Hkv, N, d, int(bool(causal)), qd, kd, vd,
-                                        _ptr(rows_a), n_rows, nthreads or default_threads())
+    rc = lib().oracle_ref_fp64_kv(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse),
+                                  B, Hq, Hkv, Nq, Nk, d, int(bool(causal)), qd, kd, vd,
+                                  _ptr(rows_a), n_rows, nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_ref_fp64 rejected its arguments")
     return out, lse

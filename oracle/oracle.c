@@ -147,7 +147,7 @@ typedef struct {
     float* out;         /* [n_rows][d]    */
     float* lse;         /* [n_rows]       (nullable) */
     uint32_t* counts;   /* [n_rows][3]    (nullable) */
-    int B, Hq, Hkv, N, d, causal, Bc, order, cast, n_sink;
+    int B, Hq, Hkv, Nq, Nk, d, causal, Bc, order, cast, n_sink;
     int scale_mode, k0;     /* k0 = log2 S (dynamic scale only) */
     float S;
     double qk_descale;  /* q_descale * k_descale (exact in double) */
@@ -178,21 +178,25 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
                      float* lse_row, uint32_t* cnt_row, float* amb_row, float* D,
                      float* P, float* F, float* o, float* blk, float* a, float* ablk)
 {
-    const int N = J->N, d = J->d, Bc = J->Bc;
-    const int64_t bh = flat / N;
-    const int r = (int)(flat % N);
+    const int Nq = J->Nq, Nk = J->Nk, d = J->d, Bc = J->Bc;
+    const int64_t bh = flat / Nq;
+    const int r = (int)(flat % Nq);
     const int b = (int)(bh / J->Hq), hq = (int)(bh % J->Hq);
     const int hk = hq / (J->Hq / J->Hkv);
     const float* qr = J->q + flat * (int64_t)d;
-    const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
-    const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
+    const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)Nk * d;
+    const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)Nk * d;
     const float S = J->S;
     /* exp(z) with z = D qd kd / sqrt(d) is exp2(D * c), D the raw dot of the
      * stored values and qd, kd the per-tensor descales of the QKV
      * quantization (Sec. 6.1); c rounded once from double */
     const float c = (float)(1.4426950408889634074 * J->qk_descale / sqrt((double)d));
 
-    const int L = J->causal ? r + 1 : N;        /* valid keys 0..L-1 */
+    /* query row r sits at key position Nk - Nq + r: the Nq queries are the
+     * last Nq positions of a sequence whose Nk keys are all cached (Nq = Nk:
+     * plain self-attention); under causal masking the row sees keys up to
+     * its own position, otherwise all Nk */
+    const int L = J->causal ? Nk - Nq + r + 1 : Nk;    /* valid keys 0..L-1 */
     const int nblk = (L + Bc - 1) / Bc;
 
     /* line: m <- -inf, l <- 0, O <- 0 (FP32) */
@@ -416,14 +420,17 @@ static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
  *   Both are [B*Hq][ceil(N/block_kv)](...) with bh = b*Hq + hq.
  * Returns 0, or -1 on an invalid argument.
  */
-int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
+int oracle_attn_full(const float* q, const float* k, const float* v, float* out,
                      float* lse, uint32_t* counts, float* amb, uint32_t* gap_hist,
-                     uint32_t* blk_zero, int nbins, int B, int Hq, int Hkv, int N, int d,
-                     int causal, int block_kv, int order, float S, int cast, int scale_mode,
-                     int n_sink, float q_descale, float k_descale, float v_descale,
-                     double amb_rel, double jitter_rel, const int64_t* rows, int64_t n_rows,
-                     int nthreads)
+                     uint32_t* blk_zero, int nbins, int B, int Hq, int Hkv, int Nq, int Nk,
+                     int d, int causal, int block_kv, int order, float S, int cast,
+                     int scale_mode, int n_sink, float q_descale, float k_descale,
+                     float v_descale, double amb_rel, double jitter_rel, const int64_t* rows,
+                     int64_t n_rows, int nthreads)
 {
+    const int N = Nq;           /* rows are indexed over the Nq queries */
+    if (Nq > Nk)
+        return -1;
     if (!(amb_rel >= 0.0) || !(amb_rel < 0.5) || !(fabs(jitter_rel) < 0.5))
         return -1;
     if ((gap_hist != NULL) != (blk_zero != NULL) || (gap_hist && (nbins < 1 || nbins > 64)))
@@ -452,7 +459,7 @@ int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
     attn_job J;
     memset(&J, 0, sizeof(J));
     J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse; J.counts = counts;
-    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
+    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.Nq = Nq; J.Nk = Nk; J.d = d; J.causal = causal;
     J.Bc = block_kv; J.order = order; J.cast = cast; J.n_sink = n_sink;
     J.scale_mode = scale_mode; J.k0 = k0;
     J.S = S; J.rows = rows; J.n_rows = n_rows; J.nthreads = nthreads;
@@ -464,13 +471,27 @@ int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
     J.gap_hist = gap_hist;
     J.blk_zero = blk_zero;
     J.nbins = nbins;
-    J.nblk_all = (N + block_kv - 1) / block_kv;
+    J.nblk_all = (Nk + block_kv - 1) / block_kv;
     if (gap_hist) {
         memset(gap_hist, 0, sizeof(uint32_t) * (size_t)B * Hq * J.nblk_all * nbins);
         memset(blk_zero, 0, sizeof(uint32_t) * (size_t)B * Hq * J.nblk_all);
     }
     run_threads(attn_worker, &J, &J.lock, nthreads);
     return 0;
+}
+
+int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
+                     float* lse, uint32_t* counts, float* amb, uint32_t* gap_hist,
+                     uint32_t* blk_zero, int nbins, int B, int Hq, int Hkv, int N, int d,
+                     int causal, int block_kv, int order, float S, int cast, int scale_mode,
+                     int n_sink, float q_descale, float k_descale, float v_descale,
+                     double amb_rel, double jitter_rel, const int64_t* rows, int64_t n_rows,
+                     int nthreads)
+{
+    return oracle_attn_full(q, k, v, out, lse, counts, amb, gap_hist, blk_zero, nbins, B, Hq,
+                            Hkv, N, N, d, causal, block_kv, order, S, cast, scale_mode, n_sink,
+                            q_descale, k_descale, v_descale, amb_rel, jitter_rel, rows, n_rows,
+                            nthreads);
 }
 
 int oracle_attn_bound(const float* q, const float* k, const float* v, float* out,
@@ -517,7 +538,7 @@ typedef struct {
     const float *q, *k, *v;
     double* out;
     double* lse;
-    int B, Hq, Hkv, N, d, causal;
+    int B, Hq, Hkv, Nq, Nk, d, causal;
     double qk_descale, v_descale;
     const int64_t* rows;
     int64_t n_rows, next;
@@ -527,8 +548,8 @@ typedef struct {
 static void* ref_worker(void* arg)
 {
     ref_job* J = (ref_job*)arg;
-    const int N = J->N, d = J->d;
-    double* z = (double*)malloc(sizeof(double) * (size_t)N);
+    const int Nq = J->Nq, Nk = J->Nk, d = J->d;
+    double* z = (double*)malloc(sizeof(double) * (size_t)Nk);
     for (;;) {
         int64_t i;
         pthread_mutex_lock(&J->lock);
@@ -537,14 +558,14 @@ static void* ref_worker(void* arg)
         if (i >= J->n_rows)
             break;
         const int64_t flat = J->rows ? J->rows[i] : i;
-        const int64_t bh = flat / N;
-        const int r = (int)(flat % N);
+        const int64_t bh = flat / Nq;
+        const int r = (int)(flat % Nq);
         const int b = (int)(bh / J->Hq), hq = (int)(bh % J->Hq);
         const int hk = hq / (J->Hq / J->Hkv);
         const float* qr = J->q + flat * (int64_t)d;
-        const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
-        const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)N * d;
-        const int L = J->causal ? r + 1 : N;
+        const float* K = J->k + ((int64_t)b * J->Hkv + hk) * (int64_t)Nk * d;
+        const float* V = J->v + ((int64_t)b * J->Hkv + hk) * (int64_t)Nk * d;
+        const int L = J->causal ? Nk - Nq + r + 1 : Nk;   /* row r at position Nk - Nq + r */
         const double scale = J->qk_descale / sqrt((double)d);
         double zmax = -INFINITY;
         for (int t = 0; t < L; t++) {
@@ -575,13 +596,13 @@ static void* ref_worker(void* arg)
     return NULL;
 }
 
-int oracle_ref_fp64_descaled(const float* q, const float* k, const float* v,
-                             double* out, double* lse, int B, int Hq, int Hkv, int N,
-                             int d, int causal, double q_descale, double k_descale,
-                             double v_descale, const int64_t* rows, int64_t n_rows,
-                             int nthreads)
+int oracle_ref_fp64_kv(const float* q, const float* k, const float* v, double* out,
+                       double* lse, int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                       double q_descale, double k_descale, double v_descale,
+                       const int64_t* rows, int64_t n_rows, int nthreads)
 {
-    if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
+    const int N = Nq;
+    if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || Nq < 1 || Nk < Nq ||
         d < 1 || Hq % Hkv != 0 || n_rows < 0)
         return -1;
     if (rows)
@@ -593,12 +614,22 @@ int oracle_ref_fp64_descaled(const float* q, const float* k, const float* v,
     ref_job J;
     memset(&J, 0, sizeof(J));
     J.q = q; J.k = k; J.v = v; J.out = out; J.lse = lse;
-    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.N = N; J.d = d; J.causal = causal;
+    J.B = B; J.Hq = Hq; J.Hkv = Hkv; J.Nq = Nq; J.Nk = Nk; J.d = d; J.causal = causal;
     J.rows = rows; J.n_rows = n_rows;
     J.qk_descale = q_descale * k_descale;
     J.v_descale = v_descale;
     run_threads(ref_worker, &J, &J.lock, nthreads);
     return 0;
+}
+
+int oracle_ref_fp64_descaled(const float* q, const float* k, const float* v,
+                             double* out, double* lse, int B, int Hq, int Hkv, int N,
+                             int d, int causal, double q_descale, double k_descale,
+                             double v_descale, const int64_t* rows, int64_t n_rows,
+                             int nthreads)
+{
+    return oracle_ref_fp64_kv(q, k, v, out, lse, B, Hq, Hkv, N, N, d, causal, q_descale,
+                              k_descale, v_descale, rows, n_rows, nthreads);
 }
 
 int oracle_ref_fp64(const float* q, const float* k, const float* v,

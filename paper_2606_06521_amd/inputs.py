@@ -279,6 +279,18 @@ def with_delta(inp: AttnInputs, delta: float) -> AttnInputs:
                       dict(inp.meta))
 
 
+def last_queries(inp: AttnInputs, nq: int) -> AttnInputs:
+    """The KV-cache prefill shape: the same keys and values, and only the last
+    ``nq`` query rows (positions N - nq .. N - 1 of the sequence)."""
+    if not 0 < nq <= inp.N:
+        raise ValueError("need 0 < nq <= N")
+    cut = slice(inp.N - nq, inp.N)
+    return AttnInputs(inp.B, inp.Hq, inp.Hkv, inp.N, inp.d, inp.fmt, inp.delta, inp.n_sink,
+                      np.ascontiguousarray(inp.q32[:, :, cut]), inp.k32, inp.v32,
+                      np.ascontiguousarray(inp.q_dev[:, :, cut]), inp.k_dev, inp.v_dev,
+                      inp.delta_eff, dict(inp.meta, nq=nq))
+
+
 def sample_rows(B: int, Hq: int, N: int, tile: int, every: int, seed: int,
                 per_tile: int = 2) -> np.ndarray:
     """Flat row ids ((b*Hq + h)*N + r) for row-sampled checks: in every head, the
