@@ -39,7 +39,9 @@ DTYPES = {"fast": "bf16 QK^T + e4m3 P.V, fp32 accumulate",
 KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast_kernel.hpp",
                   "paper_2606_06521_amd/csrc/attn_fast.hip",
                   "paper_2606_06521_amd/csrc/attn_fast_qk8.hip",
+                  "paper_2606_06521_amd/csrc/attn_prefill.hip",
                   "paper_2606_06521_amd/csrc/attn_common.hpp"]
+HBM_PEAK_GBS = 8000.0
 
 
 def traffic_file(workload: str) -> str:
@@ -93,7 +95,7 @@ def write_traffic(fetch_csv: str, write_csv: str, workload: str, copy_mib: int =
     def read(path):
         rows = list(csv.DictReader(open(path)))
         # the timed launches: causal, no counts, static power-of-two scale
-        kern = [float(r["Counter_Value"]) for r in rows if "fast_kernel" in r["Kernel_Name"]
+        kern = [float(r["Counter_Value"]) for r in rows if "_kernel<" in r["Kernel_Name"]
                 and ", true, false, 1," in r["Kernel_Name"]]
         copy = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
         return sum(kern) / len(kern), copy
@@ -136,7 +138,7 @@ def main() -> int:
     import torch
 
     from paper_2606_06521_amd import attn_fp8 as A
-    from paper_2606_06521_amd.inputs import make_inputs, sample_rows
+    from paper_2606_06521_amd.inputs import last_queries, make_inputs, sample_rows
     from paper_2606_06521_amd.workloads import HEADLINE, WORKLOADS
 
     w = WORKLOADS[args.workload or HEADLINE]
@@ -147,6 +149,8 @@ def main() -> int:
     t_gen = time.time()
     inp = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=delta, seed=w.seed_base,
                       bias_var=w.bias_var)
+    if w.nq:
+        inp = last_queries(inp, w.nq)     # w.nq queries against the w.N-key cache
     if w.fmt == "f32":
         q = torch.from_numpy(inp.q_dev).cuda()
         k = torch.from_numpy(inp.k_dev).cuda()
@@ -159,8 +163,8 @@ def main() -> int:
         q = torch.from_numpy(inp.q_dev.view(np.int16)).cuda().view(torch.bfloat16)
         k = torch.from_numpy(inp.k_dev.view(np.int16)).cuda().view(torch.bfloat16)
         v = torch.from_numpy(inp.v_dev).cuda().view(torch.float8_e4m3fn)
-    out = torch.empty((w.B, w.Hq, w.N, w.d), dtype=torch.float32, device="cuda")
-    lse = torch.empty((w.B, w.Hq, w.N), dtype=torch.float32, device="cuda")
+    out = torch.empty((w.B, w.Hq, w.rows, w.d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((w.B, w.Hq, w.rows), dtype=torch.float32, device="cuda")
     gen_s = time.time() - t_gen
 
     if args.copy_calibration_mib > 0:
@@ -178,8 +182,12 @@ def main() -> int:
     ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr())
 
     def step():
-        st = A.attn_fp8_fwd(*ptrs, w.B, w.Hq, w.Hkv, w.N, w.d, int(w.causal), w.block_kv, ordc, S,
-                            mode, sptr)
+        if w.nq:
+            st = A.attn_fp8_fwd_kv(*ptrs, w.B, w.Hq, w.Hkv, w.rows, w.N, w.d, int(w.causal),
+                                   w.block_kv, ordc, S, mode, 1.0, 1.0, 1.0, sptr)
+        else:
+            st = A.attn_fp8_fwd(*ptrs, w.B, w.Hq, w.Hkv, w.N, w.d, int(w.causal), w.block_kv,
+                                ordc, S, mode, sptr)
         if st != A.ATTN_OK:
             raise A.AttnError(st)
 
@@ -204,6 +212,12 @@ def main() -> int:
     peak = PEAK_TFLOPS["fp8"] if w.mode in ("fast", "fp8qk") else 157.3
     value = flops / (ms_per_step * 1e-3) / 1e12
     achieved = flops / (kernel_ms_avg * 1e-3) / 1e12
+    # algorithmic HBM bytes: q, k, v once, out and lse written once
+    qk_bytes = 1 if w.fmt == "e4m3" else (2 if w.fmt == "bf16_e4m3" else 4)
+    v_bytes = 4 if w.fmt == "f32" else 1
+    hbm_bytes = float(w.B * (w.Hq * w.rows * w.d * qk_bytes + w.Hkv * w.N * w.d * (qk_bytes + v_bytes)
+                             + w.Hq * w.rows * (4 * w.d + 4)))
+    hbm_bound = flops / hbm_bytes < peak / HBM_PEAK_GBS * 1e3
 
     # P-underflow diagnostic on the same inputs (timed separately, not reported as throughput)
     cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=w.causal, block_kv=w.block_kv,
@@ -225,10 +239,22 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": DTYPES[w.mode],
         "data": "synthetic (seeded sink workload, Delta=%g, 4 sink keys)" % delta,
-        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N, "d": w.d,
+        "config": {"workload": w.name, "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv, "N": w.N,
+                   "query_rows": w.rows, "d": w.d,
                    "causal": w.causal, "mode": w.mode, "block_kv": w.block_kv, "order": order,
                    "S": S, "delta_eff": round(inp.delta_eff, 4), "parallelism": "single GPU"},
         "roofline": {
+            "bound": "hbm",
+            "achieved": round(hbm_bytes / (kernel_ms_avg * 1e-3) / 1e9, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(hbm_bytes / (kernel_ms_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_per_launch": hbm_bytes,
+            "traffic": measured_traffic(w.name),
+            "kernel_ms_avg": round(kernel_ms_avg, 4),
+            "flops_per_launch": flops,
+            "tflops": round(achieved, 2),
+        } if hbm_bound else {
             "bound": "mfma",
             "achieved": round(achieved, 2),
             "peak": peak,
@@ -266,10 +292,11 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows, out_dyn_dev=No
 
     nthreads = min(16, oracle.default_threads())
     # about 10-15 s of oracle work on 16 host threads at the headline size
-    every = max(1, (w.B * w.Hq * w.N) // 524288)
-    rows = np.arange(0, w.B * w.Hq * w.N, every, dtype=np.int64)
-    rows = np.unique(np.concatenate([rows, sample_rows(w.B, w.Hq, w.N, 128, 10 ** 9, seed=0)[:64]]))
-    keys = (rows % w.N + 1) if w.causal else np.full(rows.size, w.N)
+    every = max(1, (w.B * w.Hq * w.rows) // 524288)
+    rows = np.arange(0, w.B * w.Hq * w.rows, every, dtype=np.int64)
+    rows = np.unique(np.concatenate([rows, sample_rows(w.B, w.Hq, w.rows, 128, 10 ** 9,
+                                                       seed=0)[:64]]))
+    keys = (rows % w.rows + (w.N - w.rows) + 1) if w.causal else np.full(rows.size, w.N)
     flops = float(4.0 * w.d * keys.sum())
     t0 = time.perf_counter()
     o_out, o_lse, o_cnt = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,

@@ -171,6 +171,40 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
                                         void* stream);
 
 /*
+ * Queries against a KV cache: Nq query rows per (batch, head) against Nk
+ * cached keys (0 <= Nq <= Nk), the prefill shape of the paper's Exp. 1
+ * (q_len = 32 against N = 4096) and of the prefill kernel it simulates
+ * (Sec. 6: kernel-faithful simulation).  Query row r is the token at key position
+ * Nk - Nq + r (the queries are the last Nq positions); with causal = 1 it
+ * sees keys 0 .. Nk - Nq + r, otherwise all Nk.  Algorithm 1 is unchanged:
+ * every row visits its KV blocks [j*block_kv, (j+1)*block_kv) in the given
+ * order, the P-cast and the counts follow the row's sequential running
+ * maximum exactly.
+ *
+ *   q    [B][Hq][Nq][d], k and v [B][Hkv][Nk][d] (dtypes as for the mode);
+ *   out  [B][Hq][Nq][d] float32, lse [B][Hq][Nq] (optional),
+ *   counts [B][Hq][Nq][3] (count variant).
+ *
+ * With Nq = Nk these are attn_fp8_fwd_descaled / _p_underflow_count_descaled.
+ * With Nq < Nk the fast modes run on a prefill kernel: the four waves of a
+ * workgroup split a 32-row tile's KV blocks into contiguous ranges of the
+ * visit order; each range starts from the running maximum the row reached
+ * before it, so the P codes are those of the sequential visit; only the FP32
+ * summation order of O and l differs.  Nq > Nk returns ATTN_ERR_INVALID_ARG;
+ * other arguments and return codes as for the descaled entry points.
+ */
+int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse,
+                    int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                    int block_kv, int order, float S, int mode, float q_descale,
+                    float k_descale, float v_descale, void* stream);
+
+int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, int B,
+                                  int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                                  int block_kv, int order, float S, int mode, int n_sink,
+                                  float q_descale, float k_descale, float v_descale,
+                                  uint32_t* counts, float* out, float* lse, void* stream);
+
+/*
  * Per-block diagnostic: where each KV block sits below the running maximum,
  * and how many of its P values the cast zeroes.  The paper's collapse
  * analysis assumes one sink cluster at key 0 and notes that with sinks spread

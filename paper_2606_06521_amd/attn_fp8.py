@@ -41,6 +41,11 @@ _lib.attn_fp8_fwd_descaled.restype = _I
 _lib.attn_fp8_p_underflow_count_descaled.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I]
                                                      + [_F, _F, _F, _P, _P, _P, _P])
 _lib.attn_fp8_p_underflow_count_descaled.restype = _I
+_lib.attn_fp8_fwd_kv.argtypes = [_P] * 5 + [_I] * 9 + [_F, _I, _F, _F, _F, _P]
+_lib.attn_fp8_fwd_kv.restype = _I
+_lib.attn_fp8_p_underflow_count_kv.argtypes = ([_P] * 3 + [_I] * 9 + [_F, _I, _I, _F, _F, _F]
+                                               + [_P] * 4)
+_lib.attn_fp8_p_underflow_count_kv.restype = _I
 _lib.attn_fp8_block_gap_diag.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _F, _F, _F, _I]
                                          + [_P] * 5 + [_P])
 _lib.attn_fp8_block_gap_diag.restype = _I
@@ -85,6 +90,22 @@ def attn_fp8_p_underflow_count_descaled(q, k, v, B, Hq, Hkv, N, d, causal, block
                                                     float(v_descale), counts, out, lse, stream)
 
 
+def attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S, mode,
+                    q_descale, k_descale, v_descale, stream):
+    return _lib.attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
+                                float(S), mode, float(q_descale), float(k_descale),
+                                float(v_descale), stream)
+
+
+def attn_fp8_p_underflow_count_kv(q, k, v, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S,
+                                  mode, n_sink, q_descale, k_descale, v_descale, counts, out,
+                                  lse, stream):
+    return _lib.attn_fp8_p_underflow_count_kv(q, k, v, B, Hq, Hkv, Nq, Nk, d, causal, block_kv,
+                                              order, float(S), mode, n_sink, float(q_descale),
+                                              float(k_descale), float(v_descale), counts, out,
+                                              lse, stream)
+
+
 def attn_fp8_block_gap_diag(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order, S, mode, n_sink,
                             q_descale, k_descale, v_descale, nbins, gap_hist, blk_zero, counts,
                             out, lse, stream):
@@ -112,7 +133,7 @@ def _check(q, k, v, mode):
     if q.dim() != 4 or k.dim() != 4 or v.dim() != 4:
         raise ValueError("q, k, v must be [B, H, N, d]")
     B, Hq, N, d = q.shape
-    if k.shape != v.shape or k.shape[0] != B or k.shape[2] != N or k.shape[3] != d:
+    if k.shape != v.shape or k.shape[0] != B or k.shape[2] < N or k.shape[3] != d:
         raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
     for t in (q, k, v):
         if not t.is_cuda or not t.is_contiguous():
@@ -125,7 +146,7 @@ def _check(q, k, v, mode):
             raise TypeError("fp8qk mode takes float8_e4m3fn (or uint8) q, k and v")
     elif q.dtype != torch.float32 or k.dtype != torch.float32 or v.dtype != torch.float32:
         raise TypeError("faithful / nocast modes take float32 q, k, v")
-    return B, Hq, k.shape[1], N, d
+    return B, Hq, k.shape[1], N, d, k.shape[2]
 
 
 def _ptr(t):
@@ -141,17 +162,19 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
         block_kv: int = 128, mode: str = "fast", out=None, lse=None, want_lse: bool = True,
         stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
     """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None).
+    k, v may hold more keys than q has rows (a KV cache): query row r then
+    sits at key position Nk - N + r.
     scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8);
     descales = per-tensor (q, k, v) descales of the stored values."""
     m = MODES[mode]
-    B, Hq, Hkv, N, d = _check(q, k, v, m)
+    B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
     if out is None:
         out = torch.empty((B, Hq, N, d), dtype=torch.float32, device=q.device)
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
-    st = attn_fp8_fwd_descaled(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N,
-                               d, int(bool(causal)), int(block_kv), ORDERS[order], S,
-                               m | SCALES[scale], *descales, _stream(stream))
+    st = attn_fp8_fwd_kv(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N, Nk, d,
+                         int(bool(causal)), int(block_kv), ORDERS[order], S, m | SCALES[scale],
+                         *descales, _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return out, lse
@@ -162,12 +185,12 @@ def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", caus
                       stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
     """P-underflow diagnostic; returns counts [B,Hq,N,3] uint32 (as int32 storage)."""
     m = MODES[mode]
-    B, Hq, Hkv, N, d = _check(q, k, v, m)
+    B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
     counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
-    st = attn_fp8_p_underflow_count_descaled(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d,
-                                             int(bool(causal)), int(block_kv), ORDERS[order], S,
-                                             m | SCALES[scale], int(n_sink), *descales,
-                                             _ptr(counts), _ptr(out), _ptr(lse), _stream(stream))
+    st = attn_fp8_p_underflow_count_kv(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, Nk, d,
+                                       int(bool(causal)), int(block_kv), ORDERS[order], S,
+                                       m | SCALES[scale], int(n_sink), *descales, _ptr(counts),
+                                       _ptr(out), _ptr(lse), _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return counts
@@ -179,7 +202,9 @@ def block_gap_diag(q, k, v, *, S: float = 256.0, order: str = "reverse", causal:
     """Per-block diagnostic; returns (gap_hist [B,Hq,nblk,nbins], blk_zero [B,Hq,nblk],
     counts [B,Hq,N,3]), all uint32 held in int32 storage."""
     m = MODES[mode]
-    B, Hq, Hkv, N, d = _check(q, k, v, m)
+    B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
+    if Nk != N:
+        raise ValueError("block_gap_diag takes square problems (as many keys as query rows)")
     nblk = (N + block_kv - 1) // block_kv
     hist = torch.empty((B, Hq, nblk, nbins), dtype=torch.int32, device=q.device)
     bz = torch.empty((B, Hq, nblk), dtype=torch.int32, device=q.device)

@@ -42,7 +42,9 @@ struct Params {
     uint32_t* blk_zero;
     int nbins;
     int nblk_all;        // ceil(N / block_kv)
-    int B, Hq, Hkv, N;
+    int B, Hq, Hkv, N;   // N: query rows per (batch, head)
+    int Nk;              // cached keys per (batch, kv head); N for self-attention
+    int qoff;            // Nk - N: query row r sits at key position r + qoff
     int order;           // 0 forward, 1 reverse
     int n_sink;
     float S;             // static P-scale (2^k0 with the dynamic scale)

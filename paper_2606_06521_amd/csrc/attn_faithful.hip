@@ -34,7 +34,7 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
     int bh, tile;
     if (!map_tile<CAUSAL>(p, bh, tile))
         return;
-    const int N = p.N;
+    const int N = p.N, Nk = p.Nk, qoff = p.qoff;   // query rows, keys, row r at key r + qoff
     const int b = bh / p.Hq;
     const int hq = bh - b * p.Hq;
     const int hk = hq / (p.Hq / p.Hkv);
@@ -48,7 +48,7 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
     const int row = wrow0 + n;
 
     const float* Qg = static_cast<const float*>(p.q) + (size_t)bh * N * D;
-    const size_t kvoff = ((size_t)b * p.Hkv + hk) * (size_t)N * D;
+    const size_t kvoff = ((size_t)b * p.Hkv + hk) * (size_t)Nk * D;
     const float* Kg = static_cast<const float*>(p.k) + kvoff;
     const float* Vg = static_cast<const float*>(p.v) + kvoff;
 
@@ -71,10 +71,11 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
     }
 
     const int last_row_wg = min(row0 + BM, N) - 1;
-    const int nblk = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
+    const int nblk = CAUSAL ? (last_row_wg + qoff) / BC + 1 : (Nk + BC - 1) / BC;
     const bool wave_on = wrow0 < N;
-    // every row of a wave lies in the same BC-block of rows (BC is a multiple of 32)
-    const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nblk;
+    // blocks of the wave's rows (with qoff = 0 all of them lie in one
+    // BC-block of rows; otherwise the last block may hold keys for some rows only)
+    const int nblk_w = CAUSAL ? (min(wrow0 + 31, N - 1) + qoff) / BC + 1 : nblk;
     const int a_key = a_row_to_key(n);
 
     const float c = p.c;
@@ -99,7 +100,7 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
             const int c4 = u - key * (D / 4);
             f32x4 kv = {0.f, 0.f, 0.f, 0.f};
             f32x4 vv = {0.f, 0.f, 0.f, 0.f};
-            if (t0 + key < N) {
+            if (t0 + key < Nk) {
                 kv = *reinterpret_cast<const f32x4*>(Kg + (size_t)(t0 + key) * D + 4 * c4);
                 vv = *reinterpret_cast<const f32x4*>(Vg + (size_t)(t0 + key) * D + 4 * c4);
             }
@@ -129,13 +130,13 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
         }
 
         // ---- mask: keys past the sequence end, keys after the row (causal) ----
-        if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
+        if ((CAUSAL && t0 + BC - 1 > wrow0 + qoff) || t0 + BC > Nk) {
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int key = t0 + 32 * kt + 16 * h + r;
-                    if (key >= N || (CAUSAL && key > row))
+                    if (key >= Nk || (CAUSAL && key > row + qoff))
                         s[kt][r] = -INFINITY;
                 }
         }
@@ -148,11 +149,16 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
             for (int r = 0; r < 16; ++r)
                 mx = fmax_f(mx, s[kt][r]);
         mx = fmax_f(mx, other_half(mx));
+        const bool vis = mx > -INFINITY;            // the row has a key in this block
         const float m_new = fmax_f(m_run, mx);
         const float mc_new = m_new * c;
-        const float alpha = (float)exp2((double)(mc_run - mc_new));
-        const float nmc = -mc_new;
-        if (COUNT && p.gap_hist && h == 0 && row < N)
+        // before the row's first valid key (possible only with qoff > 0 in
+        // reverse order) nothing has accumulated: alpha is irrelevant and P
+        // must be 0 (x = -inf), not NaN
+        const bool none = mc_new == -INFINITY;
+        const float alpha = none ? 1.f : (float)exp2((double)(mc_run - mc_new));
+        const float nmc = none ? 0.f : -mc_new;
+        if (COUNT && p.gap_hist && vis && h == 0 && row < N)
             record_gap(p, bh, j, mx, c, nmc);
         // Dynamic P-scale: this block's rows cast P * 2^kj, kj = k0 +
         // clamp(floor(-xmax), 0, 126 - k0) with xmax = fma(block max, c, -mc),
@@ -189,8 +195,8 @@ __global__ void __launch_bounds__(256) faithful_kernel(Params p)
                     const int code = __builtin_amdgcn_cvt_pk_fp8_f32(y0, y1, 0, false);
                     if (COUNT) {
                         const int k0 = t0 + 32 * kt + 16 * h + r;
-                        const bool z0 = (code & 0xFF) == 0 && k0 < N && (!CAUSAL || k0 <= row);
-                        const bool z1 = (code & 0xFF00) == 0 && k0 + 1 < N && (!CAUSAL || k0 + 1 <= row);
+                        const bool z0 = (code & 0xFF) == 0 && k0 < Nk && (!CAUSAL || k0 <= row + qoff);
+                        const bool z1 = (code & 0xFF00) == 0 && k0 + 1 < Nk && (!CAUSAL || k0 + 1 <= row + qoff);
                         if (j > 0) {
                             cnt2 += z0 + z1;
                         } else {

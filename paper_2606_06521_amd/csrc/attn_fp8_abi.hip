@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kVersion = 400;   // 0.4.0: per-block gap / zero-code diagnostic
+constexpr int kVersion = 500;   // 0.5.0: KV-cache prefill shape (Nq queries, Nk keys)
 
 // Clears the diagnostic's output arrays on the caller's stream (a kernel, not
 // a memset node, so the call stays safe inside a captured graph).
@@ -29,15 +29,16 @@ bool is_pow2_scale(float S)
 }
 
 // Shared validation and dispatch of both entry points.
+// N: query rows, Nk: cached keys (N for self-attention; N <= Nk, row r at key r + Nk - N)
 int run(const void* q, const void* k, const void* v, float* out, float* lse,
-        uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int d, int causal,
+        uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, int causal,
         int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
         float k_descale, float v_descale, void* stream, uint32_t* gap_hist = nullptr,
         uint32_t* blk_zero = nullptr, int nbins = 0)
 {
     const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
     const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
-    if (B < 0 || Hq < 1 || Hkv < 1 || N < 0 || Hq % Hkv != 0)
+    if (B < 0 || Hq < 1 || Hkv < 1 || N < 0 || Nk < N || Hq % Hkv != 0)
         return ATTN_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1)
         return ATTN_ERR_INVALID_ARG;
@@ -79,7 +80,10 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
     const bool fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
-    const int bm = fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
+    // queries against a longer KV cache run on the prefill kernel (fast modes)
+    const bool prefill = fast && Nk != N;
+    const int bm = prefill ? attn::prefill_rows_per_wg()
+                           : fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
     const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;
     const int64_t total = (int64_t)B * Hq * n_tiles;
     if (total > (int64_t)1 << 30)
@@ -95,7 +99,9 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.gap_hist = gap_hist;
     p.blk_zero = blk_zero;
     p.nbins = nbins;
-    p.nblk_all = (int)(((int64_t)N + block_kv - 1) / block_kv);
+    p.nblk_all = (int)(((int64_t)Nk + block_kv - 1) / block_kv);
+    p.Nk = Nk;
+    p.qoff = Nk - N;
     p.B = B;
     p.Hq = Hq;
     p.Hkv = Hkv;
@@ -124,7 +130,12 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         if (hipGetLastError() != hipSuccess)
             return ATTN_ERR_HIP;
     }
-    if (fast) {
+    if (prefill) {
+        const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
+        const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
+        e = attn::launch_prefill(p, d, block_kv, causal != 0, count, scale,
+                                 mode == ATTN_MODE_FP8QK, s);
+    } else if (fast) {
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
         const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
@@ -156,7 +167,7 @@ int attn_fp8_fwd(const void* q, const void* k, const void* v, float* out, float*
                  int Hq, int Hkv, int N, int d, int causal, int block_kv, int order, float S,
                  int mode, void* stream)
 {
-    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, N, d, causal, block_kv, order, S,
                mode, 0, 1.0f, 1.0f, 1.0f, stream);
 }
 
@@ -165,7 +176,7 @@ int attn_fp8_p_underflow_count(const void* q, const void* k, const void* v, int 
                                float S, int mode, int n_sink, uint32_t* counts, float* out,
                                float* lse, void* stream)
 {
-    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, N, d, causal, block_kv, order, S,
                mode, n_sink, 1.0f, 1.0f, 1.0f, stream);
 }
 
@@ -174,7 +185,7 @@ int attn_fp8_fwd_descaled(const void* q, const void* k, const void* v, float* ou
                           int order, float S, int mode, float q_descale, float k_descale,
                           float v_descale, void* stream)
 {
-    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, N, N, d, causal, block_kv, order, S,
                mode, 0, q_descale, k_descale, v_descale, stream);
 }
 
@@ -184,7 +195,7 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
                                         float q_descale, float k_descale, float v_descale,
                                         uint32_t* counts, float* out, float* lse, void* stream)
 {
-    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, N, d, causal, block_kv, order, S,
                mode, n_sink, q_descale, k_descale, v_descale, stream);
 }
 
@@ -198,8 +209,27 @@ int attn_fp8_block_gap_diag(const void* q, const void* k, const void* v, int B, 
         return ATTN_ERR_INVALID_ARG;
     if (B > 0 && Hq > 0 && N > 0 && (!gap_hist || !blk_zero))
         return ATTN_ERR_INVALID_ARG;
-    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, d, causal, block_kv, order, S,
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, N, N, d, causal, block_kv, order, S,
                mode, n_sink, q_descale, k_descale, v_descale, stream, gap_hist, blk_zero, nbins);
+}
+
+int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse, int B,
+                    int Hq, int Hkv, int Nq, int Nk, int d, int causal, int block_kv, int order,
+                    float S, int mode, float q_descale, float k_descale, float v_descale,
+                    void* stream)
+{
+    return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
+               S, mode, 0, q_descale, k_descale, v_descale, stream);
+}
+
+int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, int B, int Hq,
+                                  int Hkv, int Nq, int Nk, int d, int causal, int block_kv,
+                                  int order, float S, int mode, int n_sink, float q_descale,
+                                  float k_descale, float v_descale, uint32_t* counts, float* out,
+                                  float* lse, void* stream)
+{
+    return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
+               S, mode, n_sink, q_descale, k_descale, v_descale, stream);
 }
 
 const char* attn_fp8_strerror(int status)
@@ -209,7 +239,7 @@ const char* attn_fp8_strerror(int status)
         return "ok";
     case ATTN_ERR_INVALID_ARG:
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
-               "and positive, or order/mode/causal/n_sink out of range; the dynamic scale "
+               "and positive, Nq > Nk, or order/mode/causal/n_sink out of range; the dynamic scale "
                "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive; "
                "the block diagnostic needs all three arrays and 1 <= nbins <= 64)";
     case ATTN_ERR_UNSUPPORTED:

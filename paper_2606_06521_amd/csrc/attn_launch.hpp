@@ -18,4 +18,10 @@ hipError_t launch_fast_qk8(const Params& p, int grid, int d, int block_kv, bool 
                            int scale /* kScale* */, hipStream_t stream);
 int fast_rows_per_wg(int d, int block_kv);
 
+// queries against a longer KV cache (p.Nk > p.N), fast modes: one workgroup
+// per (batch, head, 32-row query tile), grid p.per_xcd * 8
+hipError_t launch_prefill(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
+                          bool qk8, hipStream_t stream);
+int prefill_rows_per_wg();
+
 }  // namespace attn

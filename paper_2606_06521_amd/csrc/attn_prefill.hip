@@ -1,0 +1,468 @@
+// KV-cache prefill kernel (fast modes): Nq query rows against Nk cached keys,
+// query row r at key position Nk - Nq + r (causal rows see keys up to their
+// position).  The shape of the paper's Exp. 1 (q_len = 32 against N = 4096)
+// and of a prefill kernel working on a KV cache.
+//
+// A tile of 32 query rows has only 32 rows of work per KV block, so one wave
+// would run the whole key sequence alone.  Here the four waves of a workgroup
+// share the tile's KV blocks instead -- wave w takes a contiguous range of
+// the visit order -- without changing what Algorithm 1 computes:
+//   pass 1: each wave takes the row maxima of its blocks' scores; the
+//           running maximum a row has reached when its visit enters wave w's
+//           range is the maximum over the ranges of waves 0..w-1;
+//   pass 2: each wave runs Algorithm 1 over its range starting from that
+//           running maximum, so every block sees exactly the running maximum
+//           of the sequential visit: P = exp2(fma(D, c, -mc)) and its E4M3
+//           code are those of the one-wave kernel (counts included);
+//   merge:  the four (O, l) partials are brought to the row's final maximum
+//           (one exp2 each) and summed.  Only the FP32 rounding of O and l
+//           differs from the sequential chain of alpha products.
+// The scores are computed twice (once per pass); the second read of K comes
+// from L2.
+//
+// K fragments (the S^T MFMA's A operand) are read straight from HBM, 16
+// bytes per lane, in the key order of a_row_to_key.  Each wave stages the V
+// block it multiplies in its own LDS region, in the XOR-swizzled layout read
+// transposed by ds_read_b64_tr_b8 (as in the fast kernel).
+#include "attn_common.hpp"
+#include "attn_launch.hpp"
+
+#include <math.h>
+#include <type_traits>
+
+namespace attn {
+
+namespace {
+
+typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+
+__device__ inline i32x2 read_tr8(const uint8_t* p)
+{
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) i32x2*)(p));
+}
+
+constexpr int kPrefillWaves = 4;
+
+}  // namespace
+
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8>
+__global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
+{
+    constexpr int NW = kPrefillWaves;
+    constexpr int KT = BC / 32;                 // 32-key S^T tiles per block
+    constexpr int DK = QK8 ? D / 64 : D / 16;   // S^T MFMA k-steps over d
+    constexpr int DT = D / 32;                  // 32-wide d tiles of O^T
+    constexpr int PVS = BC / 64;                // 64-key FP8 MFMA k-steps
+    constexpr int KROW = QK8 ? D : 2 * D;       // bytes per Q / K row
+    constexpr int QSTEP = QK8 ? 64 : 32;        // bytes of a row per k-step
+    constexpr int VROW = D;                     // bytes per V row
+    constexpr int VCPR = VROW / 16;             // 16-byte chunks per V row
+    constexpr int V_BYTES = BC * VROW;          // one wave's V stage
+    constexpr int V_NI = V_BYTES / 1024;        // 16-byte-per-lane rounds per stage
+    constexpr int V_RPI = 1024 / VROW;          // V rows per round
+    constexpr int MERGE_BYTES = NW * 32 * D * 4;
+    constexpr int LDS_BYTES = NW * V_BYTES > MERGE_BYTES ? NW * V_BYTES : MERGE_BYTES;
+    using QFrag = std::conditional_t<QK8, i32x8, bf16x8>;
+
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+    __shared__ float tab[NW][32];     // pass 1: each wave's row maxima
+    __shared__ float lsh[NW][32];     // merge: each wave's l, at the final maximum
+    __shared__ uint32_t csh[32][3];   // merge: counts
+
+    int bh, tile;
+    if (!map_tile<false>(p, bh, tile))
+        return;
+    const int Nq = p.N, Nk = p.Nk, qoff = p.qoff;
+    const int b = bh / p.Hq;
+    const int hq = bh - b * p.Hq;
+    const int hk = hq / (p.Hq / p.Hkv);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = lane & 31;
+    const int h = lane >> 5;
+    const int row = 32 * tile + n;              // every wave holds the same 32 rows
+    const int pos = row + qoff;                 // the row's key position
+    const int rlast = min(32 * tile + 31, Nq - 1);
+    // blocks the tile visits, and this wave's contiguous range of the visit order
+    const int nbt = CAUSAL ? (rlast + qoff) / BC + 1 : (Nk + BC - 1) / BC;
+    const int it0 = nbt * w / NW, it1 = nbt * (w + 1) / NW;
+    auto jof = [&](int it) __attribute__((always_inline)) { return p.order == 0 ? it : nbt - 1 - it; };
+
+    const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * Nq * KROW;
+    const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)Nk;
+    const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
+    const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * VROW;
+
+    if (tid < 32 * 3)
+        csh[tid / 3][tid % 3] = 0u;
+
+    // Q^T fragments (B operand), as in the fast kernel
+    QFrag qf[DK];
+    if (row < Nq) {
+        const uint8_t* qr = Qg + (size_t)row * KROW;
+#pragma unroll
+        for (int kk = 0; kk < DK; ++kk)
+            qf[kk] = *reinterpret_cast<const QFrag*>(qr + QSTEP * kk + (QSTEP / 2) * h);
+    } else {
+#pragma unroll
+        for (int kk = 0; kk < DK; ++kk)
+            qf[kk] = QFrag{};
+    }
+
+    // ---- S^T = K_j Q^T, K fragments from HBM (key 32 kt + a_row_to_key(n)) ----
+    const int a_key = a_row_to_key(n);
+    f32x16 s[KT];
+    auto qk = [&](int j) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        const uint8_t* krow[KT];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+            krow[kt] = Kg + (size_t)min(t0 + 32 * kt + a_key, Nk - 1) * KROW + (QSTEP / 2) * h;
+        auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
+            return *reinterpret_cast<const QFrag*>(krow[kt] + QSTEP * kk);
+        };
+        QFrag a[2][KT];
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+            a[0][kt] = kfrag(0, kt);
+#pragma unroll
+        for (int kk = 0; kk < DK; ++kk) {
+            if (kk + 1 < DK) {
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+                    a[(kk + 1) & 1][kt] = kfrag(kk + 1, kt);
+            }
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                const f32x16 acc = kk == 0 ? f32x16{} : s[kt];
+                if constexpr (QK8)
+                    s[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[kk & 1][kt], qf[kk], acc,
+                                                                            0, 0, 0, 0, 0, 0);
+                else
+                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk & 1][kt], qf[kk], acc, 0, 0, 0);
+            }
+        }
+    };
+    // keys past the cache end or past the row's position become -inf
+    auto mask = [&](int j) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        if ((CAUSAL && t0 + BC - 1 > 32 * tile + qoff) || t0 + BC > Nk) {
+            const int lim = (CAUSAL ? min(pos, Nk - 1) : Nk - 1) - t0 - 16 * h;
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const uint32_t m = (uint32_t)((lim - (32 * kt + r)) >> 31);
+                    s[kt][r] = __uint_as_float((__float_as_uint(s[kt][r]) & ~m) | (0xFF800000u & m));
+                }
+        }
+    };
+    auto row_max = [&]() __attribute__((always_inline)) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                mx = fmax_f(mx, s[kt][r]);
+        return halves_max(mx);
+    };
+
+    // ---- pass 1: row maxima over this wave's blocks ----
+    float m1 = -INFINITY;
+    for (int it = it0; it < it1; ++it) {
+        const int j = jof(it);
+        qk(j);
+        mask(j);
+        m1 = fmax_f(m1, row_max());
+    }
+    if (h == 0)
+        tab[w][n] = m1;
+    __syncthreads();
+    float m_start = -INFINITY, m_final = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < NW; ++v) {
+        if (v < w)
+            m_start = fmax_f(m_start, tab[v][n]);
+        m_final = fmax_f(m_final, tab[v][n]);
+    }
+
+    // ---- pass 2: Algorithm 1 over this wave's range, from the running maximum m_start ----
+    const float c = p.c;
+    const float S = p.S;
+    const float inv_S = p.inv_S;
+    float m_run = m_start;
+    float mc_run = m_start * c;
+    float ell = 0.f;
+    f32x16 o[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            o[dt][r] = 0.f;
+    uint32_t pk[KT][4] = {};
+    int pv_sb = 127;
+    uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
+
+    uint8_t* vst = lds + w * V_BYTES;
+    auto vswz = [](int r) __attribute__((always_inline)) { return ((r / (256 / VROW)) & (VCPR / 2 - 1)) * 2; };
+    const int j16 = n & 15;
+    const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
+                                       8 * (j16 & 1));
+    // V_j -> this wave's LDS stage: round i writes LDS bytes [1024 i, +1024);
+    // lane l fills row i V_RPI + l / VCPR at physical chunk l % VCPR, which
+    // holds logical chunk (l % VCPR) ^ vswz(row)
+    auto stage_v = [&](int j) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        i32x4 tmp[V_NI];
+#pragma unroll
+        for (int i = 0; i < V_NI; ++i) {
+            const int rv = i * V_RPI + lane / VCPR;
+            const int lc = (lane % VCPR) ^ vswz(rv);
+            tmp[i] = *reinterpret_cast<const i32x4*>(Vg + (size_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc);
+        }
+#pragma unroll
+        for (int i = 0; i < V_NI; ++i)
+            *reinterpret_cast<i32x4*>(vst + 1024 * i + 16 * lane) = tmp[i];
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    };
+
+    for (int it = it0; it < it1; ++it) {
+        const int j = jof(it);
+        const int t0 = j * BC;
+        qk(j);
+        mask(j);
+        const float mx = row_max();
+        const bool vis = mx > -INFINITY;            // the row has a key in this block
+        const float m_new = fmax_f(m_run, mx);
+        const float mc_new = m_new * c;
+        // before the row's first valid key nothing has accumulated: alpha is
+        // irrelevant and P must be 0 (x = -inf), not NaN
+        const bool none = mc_new == -INFINITY;
+        const float alpha = none ? 1.f : __builtin_amdgcn_exp2f(mc_run - mc_new);
+        const float nmc = none ? 0.f : -mc_new;
+        if (COUNT && p.gap_hist && vis && h == 0 && row < Nq)
+            record_gap(p, bh, j, mx, c, nmc);
+        float cvt_scale = inv_S;
+        if constexpr (SCALE == kScaleDynamic) {
+            const float xmax = __builtin_fmaf(mx, c, nmc);
+            const float f = __builtin_fminf(__builtin_fmaxf(__builtin_floorf(-xmax), 0.f),
+                                            (float)(126 - p.k0));
+            const int kj = p.k0 + (int)f;
+            cvt_scale = __uint_as_float((uint32_t)(127 - kj) << 23);
+            pv_sb = 127 + p.k0 - kj;
+        }
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                s[kt][r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s[kt][r], c, nmc));
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                o[dt][r] *= alpha;
+        float lsum = 0.f;
+        uint32_t bz = 0;
+#pragma unroll
+        for (int kt = 0; kt < KT; ++kt) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                lsum += s[kt][r];
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                const float p0 = s[kt][4 * r4 + 0], p1 = s[kt][4 * r4 + 1];
+                const float p2 = s[kt][4 * r4 + 2], p3 = s[kt][4 * r4 + 3];
+                uint32_t word;
+                if constexpr (SCALE != kScaleAny) {
+                    s16x2 lo = __builtin_bit_cast(s16x2, pk[kt][r4]);
+                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p0, p1, cvt_scale, false);
+                    lo = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(lo, p2, p3, cvt_scale, true);
+                    word = __builtin_bit_cast(uint32_t, lo);
+                } else {
+                    int wv = __builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(p0 * S, 448.f),
+                                                            __builtin_fminf(p1 * S, 448.f),
+                                                            (int)pk[kt][r4], false);
+                    wv = __builtin_amdgcn_cvt_pk_fp8_f32(__builtin_fminf(p2 * S, 448.f),
+                                                        __builtin_fminf(p3 * S, 448.f), wv, true);
+                    word = (uint32_t)wv;
+                }
+                pk[kt][r4] = word;
+                if (COUNT) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
+                        const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < Nk &&
+                                       (!CAUSAL || key <= pos) && row < Nq;
+                        if (z) {
+                            if (j > 0) ++cnt2;
+                            else if (key < p.n_sink) ++cnt0;
+                            else ++cnt1;
+                            ++bz;
+                        }
+                    }
+                }
+            }
+        }
+        ell = alpha * ell + lsum;
+        if (COUNT && p.blk_zero)
+            record_block_zeros(p, bh, j, bz);
+        m_run = m_new;
+        mc_run = mc_new;
+
+        // O^T += V_j^T P8^T
+        stage_v(j);
+#pragma unroll
+        for (int i = 0; i < PVS * DT; ++i) {
+            const int js = i / DT, dt = i % DT;
+            const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
+            const i32x2 r0 = read_tr8(va);
+            const i32x2 r1 = read_tr8(va + 8 * VROW);
+            const i32x2 r2 = read_tr8(va + 32 * VROW);
+            const i32x2 r3 = read_tr8(va + 40 * VROW);
+            const i32x8 av = {r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+            i32x8 bop;
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+                bop[q4] = (int)pk[2 * js][q4];
+                bop[4 + q4] = (int)pk[2 * js + 1][q4];
+            }
+            if constexpr (SCALE == kScaleDynamic)
+                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bop, o[dt], 0, 0, 0, 127, 0, pv_sb);
+            else
+                o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bop, o[dt], 0, 0, 0, 0, 0, 0);
+        }
+    }
+
+    // ---- merge: bring each wave's (O, l) to the row's final maximum and sum ----
+    const float mc_final = m_final * c;
+    const float beta = mc_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mc_run - mc_final);
+    const float ell_w = (ell + other_half(ell)) * beta;
+    if (COUNT) {
+        cnt0 += other_half_u32(cnt0);
+        cnt1 += other_half_u32(cnt1);
+        cnt2 += other_half_u32(cnt2);
+    }
+    __syncthreads();                                   // V stages free for the merge buffer
+    float* mbuf = reinterpret_cast<float*>(lds) + w * 32 * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+            f32x4 v4;
+            v4[0] = o[dt][4 * r4 + 0] * beta;
+            v4[1] = o[dt][4 * r4 + 1] * beta;
+            v4[2] = o[dt][4 * r4 + 2] * beta;
+            v4[3] = o[dt][4 * r4 + 3] * beta;
+            *reinterpret_cast<f32x4*>(mbuf + n * D + 32 * dt + 8 * r4 + 4 * h) = v4;
+        }
+    if (h == 0) {
+        lsh[w][n] = ell_w;
+        if (COUNT) {
+            atomicAdd(&csh[n][0], cnt0);
+            atomicAdd(&csh[n][1], cnt1);
+            atomicAdd(&csh[n][2], cnt2);
+        }
+    }
+    __syncthreads();
+    const float* mb = reinterpret_cast<const float*>(lds);
+    for (int e = tid; e < 32 * D / 4; e += 64 * NW) {
+        const int rr = e / (D / 4);
+        const int grow = 32 * tile + rr;
+        if (grow >= Nq)
+            continue;
+        float l = 0.f;
+#pragma unroll
+        for (int v = 0; v < NW; ++v)
+            l += lsh[v][rr];
+        f32x4 acc = *reinterpret_cast<const f32x4*>(mb + 4 * e);
+#pragma unroll
+        for (int v = 1; v < NW; ++v) {
+            const f32x4 t = *reinterpret_cast<const f32x4*>(mb + v * 32 * D + 4 * e);
+            acc[0] += t[0];
+            acc[1] += t[1];
+            acc[2] += t[2];
+            acc[3] += t[3];
+        }
+        const size_t flat = (size_t)bh * Nq + grow;
+        if (p.out) {
+            const float inv = p.v_descale / (S * l);
+            f32x4 v4;
+            v4[0] = acc[0] * inv;
+            v4[1] = acc[1] * inv;
+            v4[2] = acc[2] * inv;
+            v4[3] = acc[3] * inv;
+            *reinterpret_cast<f32x4*>(p.out + flat * D + 4 * (e % (D / 4))) = v4;
+        }
+    }
+    if (tid < 32 && 32 * tile + tid < Nq) {
+        const size_t flat = (size_t)bh * Nq + 32 * tile + tid;
+        float l = 0.f;
+#pragma unroll
+        for (int v = 0; v < NW; ++v)
+            l += lsh[v][tid];
+        if (p.lse) {
+            float mf = -INFINITY;
+#pragma unroll
+            for (int v = 0; v < NW; ++v)
+                mf = fmax_f(mf, tab[v][tid]);
+            p.lse[flat] = (mf * c + __builtin_log2f(l)) * 0.6931471805599453f;
+        }
+        if (COUNT) {
+            p.counts[3 * flat + 0] = csh[tid][0];
+            p.counts[3 * flat + 1] = csh[tid][1];
+            p.counts[3 * flat + 2] = csh[tid][2];
+        }
+    }
+}
+
+namespace {
+
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE>
+hipError_t launch_one(const Params& p, bool qk8, hipStream_t s)
+{
+    const int grid = p.per_xcd * kNumXcd;
+    if (qk8)
+        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, true>), dim3(grid),
+                           dim3(64 * kPrefillWaves), 0, s, p);
+    else
+        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, false>), dim3(grid),
+                           dim3(64 * kPrefillWaves), 0, s, p);
+    return hipGetLastError();
+}
+
+template <int D, int BC, bool CAUSAL, bool COUNT>
+hipError_t launch_scale(const Params& p, int scale, bool qk8, hipStream_t s)
+{
+    if (scale == kScaleDynamic)
+        return launch_one<D, BC, CAUSAL, COUNT, kScaleDynamic>(p, qk8, s);
+    if (scale == kScalePow2)
+        return launch_one<D, BC, CAUSAL, COUNT, kScalePow2>(p, qk8, s);
+    return launch_one<D, BC, CAUSAL, COUNT, kScaleAny>(p, qk8, s);
+}
+
+template <int D, int BC>
+hipError_t launch_d_bc(const Params& p, bool causal, bool count, int scale, bool qk8, hipStream_t s)
+{
+    if (causal)
+        return count ? launch_scale<D, BC, true, true>(p, scale, qk8, s)
+                     : launch_scale<D, BC, true, false>(p, scale, qk8, s);
+    return count ? launch_scale<D, BC, false, true>(p, scale, qk8, s)
+                 : launch_scale<D, BC, false, false>(p, scale, qk8, s);
+}
+
+}  // namespace
+
+hipError_t launch_prefill(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
+                          bool qk8, hipStream_t stream)
+{
+    if (d == 64)
+        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, scale, qk8, stream)
+                              : launch_d_bc<64, 128>(p, causal, count, scale, qk8, stream);
+    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, scale, qk8, stream)
+                          : launch_d_bc<128, 128>(p, causal, count, scale, qk8, stream);
+}
+
+int prefill_rows_per_wg() { return 32; }
+
+}  // namespace attn

@@ -24,6 +24,11 @@ class Workload:
     orders: tuple
     bias_var: float = 0.0
     seed_base: int = 0
+    nq: int = 0               # query rows against N cached keys (0: all N rows)
+
+    @property
+    def rows(self) -> int:
+        return self.nq or self.N
 
     @property
     def fmt(self) -> str:
@@ -32,9 +37,14 @@ class Workload:
         return "f32" if self.mode in ("faithful", "nocast") else "bf16_e4m3"
 
     def flops(self) -> float:
-        """FlashAttention convention: 4*B*Hq*N^2*d, halved under causal masking."""
-        f = 4.0 * self.B * self.Hq * self.N * self.N * self.d
-        return f / 2 if self.causal else f
+        """FlashAttention convention: 4*B*Hq*N^2*d, halved under causal masking.
+        With nq query rows against N cached keys: 4 d per (row, visible key)."""
+        if not self.nq:
+            f = 4.0 * self.B * self.Hq * self.N * self.N * self.d
+            return f / 2 if self.causal else f
+        keys = (self.nq * (self.N - self.nq) + self.nq * (self.nq + 1) / 2 if self.causal
+                else self.nq * self.N)
+        return 4.0 * self.B * self.Hq * keys * self.d
 
 
 WORKLOADS = {
@@ -58,6 +68,12 @@ WORKLOADS = {
         # causal GQA 32/8 heads at 128k, Delta = 10 plus a N(0, 0.5) per-key bias
         Workload("causal_gqa_h32kv8_n131072_d128_fast_bias", 1, 32, 8, 131072, 128, True, "fast",
                  128, (10.0,), (256.0,), ("reverse",), bias_var=0.5, seed_base=20260500),
+        # Exp. 1's shape: 32 new queries against a 4096-key cache, 64 problems
+        Workload("prefill_q32_b64_n4096_d128_fast", 64, 1, 1, 4096, 128, True, "fast", 128,
+                 (7.0,), (256.0,), ("reverse",), seed_base=20260600, nq=32),
+        # a serving-sized prefill chunk: 256 queries against a 32k cache, GQA 32/8
+        Workload("prefill_q256_b4_h32kv8_n32768_d128_fast", 4, 32, 8, 32768, 128, True, "fast",
+                 128, (9.0,), (256.0,), ("reverse",), seed_base=20260700, nq=256),
     ]
 }
 

@@ -26,7 +26,8 @@ def declared_functions():
 def test_exports_every_declared_symbol(A):
     names = declared_functions()
     assert names == ["attn_fp8_block_gap_diag", "attn_fp8_fwd", "attn_fp8_fwd_descaled",
-                     "attn_fp8_p_underflow_count", "attn_fp8_p_underflow_count_descaled",
+                     "attn_fp8_fwd_kv", "attn_fp8_p_underflow_count",
+                     "attn_fp8_p_underflow_count_descaled", "attn_fp8_p_underflow_count_kv",
                      "attn_fp8_strerror", "attn_fp8_version"]
     lib = ctypes.CDLL(A.LIB_PATH)
     for n in names:
@@ -144,3 +145,21 @@ def test_block_gap_diag_validates_before_any_launch(A):
     assert g(qd=0.0) == -1
     assert g(d=32) == -2
     assert g(N=0, q=None, k=None, v=None, hist=None, bz=None, counts=None) == 0
+
+
+def test_kv_entry_points_validate(A):
+    def f(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, B=1, Hq=2, Hkv=1, Nq=32, Nk=4096, d=128,
+                 causal=1, block_kv=128, order=1, S=256.0, mode=1)
+        a.update(kw)
+        return A.attn_fp8_fwd_kv(a["q"], a["k"], a["v"], a["out"], None, a["B"], a["Hq"],
+                                 a["Hkv"], a["Nq"], a["Nk"], a["d"], a["causal"], a["block_kv"],
+                                 a["order"], a["S"], a["mode"], 1.0, 1.0, 1.0, None)
+    assert f(Nq=4097) == -1            # more queries than keys
+    assert f(Nk=-1) == -1
+    assert f(out=None) == -1
+    assert f(d=96) == -2
+    assert f(Nq=0, q=None, k=None, v=None, out=None) == 0
+    cnt = A.attn_fp8_p_underflow_count_kv(FAKE, FAKE, FAKE, 1, 2, 1, 32, 4096, 128, 1, 128, 1,
+                                          256.0, 1, 4, 1.0, 1.0, 1.0, None, None, None, None)
+    assert cnt == -1

@@ -1,0 +1,86 @@
+"""Queries against a KV cache (Nq < Nk) on the device against the oracle:
+the prefill kernel (fast modes) and the faithful kernel with a query offset.
+Same bar as the square problems: counts exact where claimed, outputs within
+the mode's tolerance (plus the code-ambiguity bound in the fast modes), lse
+within 1e-4."""
+import itertools
+
+import numpy as np
+import pytest
+
+from paper_2606_06521_amd.inputs import last_queries, make_inputs
+from paper_2606_06521_amd.workloads import WORKLOADS
+from tests.gpu_helpers import compare, log, run_gpu, to_device
+
+pytestmark = pytest.mark.gpu
+
+FMT = {"faithful": "f32", "nocast": "f32", "fast": "bf16_e4m3", "fp8qk": "e4m3"}
+
+
+@pytest.mark.parametrize("mode", ["fast", "fp8qk", "faithful"])
+@pytest.mark.parametrize("d,bkv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_small(mode, d, bkv):
+    full = make_inputs(2, 4, 2, 333, d, fmt=FMT[mode], delta=9.0, seed=900 + d + bkv)
+    for nq in (1, 32, 77):
+        inp = last_queries(full, nq)
+        dev = to_device(inp)
+        for (causal, order), (S, scale) in itertools.product(
+                itertools.product([False, True], ["forward", "reverse"]),
+                [(256.0, "static"), (448.0, "static"), (16.0, "dynamic")]):
+            label = f"kv {mode} nq={nq} nk=333 d={d} bkv={bkv} causal={causal} {order} S={S} {scale}"
+            log(label)
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale=scale)
+            compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
+
+
+def test_nocast_and_descales():
+    full = make_inputs(1, 2, 1, 300, 128, fmt="f32", delta=7.0, seed=950)
+    inp = last_queries(full, 40)
+    dev = to_device(inp)
+    for causal in (False, True):
+        label = f"kv nocast causal={causal}"
+        log(label)
+        gpu = run_gpu(dev, "nocast", 256.0, "forward", causal, 64)
+        compare(inp, gpu, "nocast", 256.0, "forward", causal, 64, label=label)
+    full8 = make_inputs(1, 4, 2, 300, 128, fmt="e4m3", delta=7.0, seed=951)
+    inp8 = last_queries(full8, 50)
+    dev8 = to_device(inp8)
+    ds = (0.75, 1.5, 2.0)
+    label = "kv fp8qk descales"
+    log(label)
+    gpu = run_gpu(dev8, "fp8qk", 256.0, "reverse", True, 128, descales=ds)
+    compare(inp8, gpu, "fp8qk", 256.0, "reverse", True, 128, label=label, descales=ds)
+
+
+@pytest.mark.parametrize("order", ["forward", "reverse"])
+def test_exp1_prefill_shape_all_rows(order):
+    # Exp. 1's shape (q_len = 32 against N = 4096, 64 problems) in full
+    w = WORKLOADS["prefill_q32_b64_n4096_d128_fast"]
+    full = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    inp = last_queries(full, w.nq)
+    dev = to_device(inp)
+    for S in (256.0, 1.0):
+        label = f"{w.name} S={S} {order}"
+        log(label)
+        gpu = run_gpu(dev, w.mode, S, order, w.causal, w.block_kv)
+        res = compare(inp, gpu, w.mode, S, order, w.causal, w.block_kv, label=label)
+        log(str(res))
+        if order == "reverse" and S == 256.0:
+            assert gpu[2][..., 2].sum() == 0, label
+
+
+def test_square_call_through_kv_entry_is_unchanged():
+    # Nq = Nk through the KV entry point runs the square kernels: bit-identical
+    from paper_2606_06521_amd import attn_fp8 as A
+    import torch
+    inp = make_inputs(1, 4, 2, 300, 128, fmt="bf16_e4m3", delta=8.0, seed=952)
+    q, k, v = to_device(inp)
+    o1, l1 = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
+    o2 = torch.empty_like(o1)
+    l2 = torch.empty_like(l1)
+    st = A.attn_fp8_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o2.data_ptr(), l2.data_ptr(),
+                           1, 4, 2, 300, 300, 128, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0,
+                           torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert st == 0
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
