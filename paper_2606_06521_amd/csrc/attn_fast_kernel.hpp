@@ -128,7 +128,10 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         const int tile = half == 0 ? T - 1 - pr : pr;
         if (half == 1 && tile == T - 1 - pr)
             break;                                    // odd tile count: the middle tile is alone
-        const int N = p.N;
+        // N query rows; Nk keys; row r at key position r + qoff (qoff = 0 for
+        // self-attention; otherwise a multiple of BC, so that every row of a
+        // wave still lies in one BC-block of key positions)
+        const int N = p.N, Nk = p.Nk, qoff = p.qoff;
         const int b = bh / p.Hq;
         const int hq = bh - b * p.Hq;
         const int hk = hq / (p.Hq / p.Hkv);
@@ -143,15 +146,15 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         const int row = wrow0 + n;
 
         const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * N * KROW;
-        const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)N;
+        const size_t kvrow0 = ((size_t)b * p.Hkv + hk) * (size_t)Nk;
         const uint8_t* Kg = static_cast<const uint8_t*>(p.k) + kvrow0 * KROW;
         const uint8_t* Vg = static_cast<const uint8_t*>(p.v) + kvrow0 * D;
 
         const int last_row_wg = min(row0 + BM, N) - 1;
-        const int nb = CAUSAL ? last_row_wg / BC + 1 : (N + BC - 1) / BC;
+        const int nb = CAUSAL ? (last_row_wg + qoff) / BC + 1 : (Nk + BC - 1) / BC;
         const bool wave_on = wrow0 < N;
         // every row of a wave lies in one BC-block of rows (BC is a multiple of 32)
-        const int nblk_w = CAUSAL ? min(wrow0 + 31, N - 1) / BC + 1 : nb;
+        const int nblk_w = CAUSAL ? (min(wrow0 + 31, N - 1) + qoff) / BC + 1 : nb;
         auto jof = [&](int k) __attribute__((always_inline)) { return p.order == 0 ? k : nb - 1 - k; };
         auto valid = [&](int k) __attribute__((always_inline)) { return k >= 0 && k < nb && wave_on && jof(k) < nblk_w; };
 
@@ -163,7 +166,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         // (4 K_RPI is a power of two >= 16, so the two key parts have disjoint
         // bits and the swizzle does not depend on it).  V likewise with
         // key = row.  Keys past the end of the sequence (only in a ragged last
-        // block) read row N-1: they are masked to P = 0 before they can contribute.
+        // block) read row Nk-1: they are masked to P = 0 before they can contribute.
         const int wl = w & 3;
         int k_key_l, v_key_l;
         uint32_t k_chunk_l, v_chunk_l;
@@ -179,7 +182,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
         auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
             const int t0 = j * BC;
-            if (t0 + BC <= N) {
+            if (t0 + BC <= Nk) {
 #pragma unroll
                 for (int it = 0; it < K_NI; ++it)
                     g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
@@ -187,21 +190,21 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             } else {
 #pragma unroll
                 for (int it = 0; it < K_NI; ++it) {
-                    const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, N - 1);
+                    const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, Nk - 1);
                     g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
                 }
             }
         };
         auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
             const int t0 = j * BC;
-            if (t0 + BC <= N) {
+            if (t0 + BC <= Nk) {
 #pragma unroll
                 for (int it = 0; it < V_NI; ++it)
                     g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
             } else {
 #pragma unroll
                 for (int it = 0; it < V_NI; ++it) {
-                    const int key = min(t0 + 4 * V_RPI * it + v_key_l, N - 1);
+                    const int key = min(t0 + 4 * V_RPI * it + v_key_l, Nk - 1);
                     g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
                 }
             }
@@ -342,10 +345,10 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         // ---- running max, alpha, P, l (pre-cast), E4M3 cast, rescale of O ----
         auto softmax = [&](int j) __attribute__((always_inline)) {
             const int t0 = j * BC;
-            if ((CAUSAL && j == nblk_w - 1) || t0 + BC > N) {
+            if ((CAUSAL && j == nblk_w - 1) || t0 + BC > Nk) {
                 // key t0 + 32 kt + 16 h + r is valid iff 32 kt + r <= lim; masked
                 // scores become -inf through a sign-mask bit select (no compares)
-                const int lim = (CAUSAL ? min(row, N - 1) : N - 1) - t0 - 16 * h;
+                const int lim = (CAUSAL ? min(row + qoff, Nk - 1) : Nk - 1) - t0 - 16 * h;
 #pragma unroll
                 for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
@@ -463,8 +466,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
 #pragma unroll
                         for (int i = 0; i < 4; ++i) {
                             const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
-                            const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < N &&
-                                           (!CAUSAL || key <= row);
+                            const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < Nk &&
+                                           (!CAUSAL || key <= row + qoff);
                             if (z) {
                                 if (j > 0) ++cnt2;
                                 else if (key < p.n_sink) ++cnt0;

@@ -80,8 +80,12 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
     const bool fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
-    // queries against a longer KV cache run on the prefill kernel (fast modes)
-    const bool prefill = fast && Nk != N;
+    // Queries against a longer KV cache (fast modes): long query chunks whose
+    // offset Nk - N is a multiple of the block run on the persistent kernel
+    // (every 32-row wave then still lies in one block of key positions);
+    // short ones, or unaligned offsets, on the prefill kernel, whose waves
+    // share a 32-row tile's KV blocks.
+    const bool prefill = fast && Nk != N && (N < 128 || (Nk - N) % block_kv != 0);
     const int bm = prefill ? attn::prefill_rows_per_wg()
                            : fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
     const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;

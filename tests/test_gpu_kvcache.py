@@ -33,6 +33,24 @@ def test_small(mode, d, bkv):
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
+@pytest.mark.parametrize("mode", ["fast", "fp8qk"])
+@pytest.mark.parametrize("bkv", [64, 128])
+def test_long_chunks(mode, bkv):
+    # 256 queries with a block-aligned offset (Nk = 640) take the persistent
+    # kernel; 200 queries at offset 133 (Nk = 333) the prefill kernel
+    for nk, nq in ((640, 256), (333, 200)):
+        full = make_inputs(1, 4, 2, nk, 128, fmt=FMT[mode], delta=9.0, seed=960 + nk + bkv)
+        inp = last_queries(full, nq)
+        dev = to_device(inp)
+        for (causal, order), (S, scale) in itertools.product(
+                itertools.product([False, True], ["forward", "reverse"]),
+                [(256.0, "static"), (448.0, "static"), (16.0, "dynamic")]):
+            label = f"kv {mode} nq={nq} nk={nk} bkv={bkv} causal={causal} {order} S={S} {scale}"
+            log(label)
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale=scale)
+            compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
+
+
 def test_nocast_and_descales():
     full = make_inputs(1, 2, 1, 300, 128, fmt="f32", delta=7.0, seed=950)
     inp = last_queries(full, 40)
