@@ -186,7 +186,7 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
  *   counts [B][Hq][Nq][3] (count variant).
  *
  * With Nq = Nk these are attn_fp8_fwd_descaled / _p_underflow_count_descaled.
- * With Nq < Nk the fast modes run on a prefill kernel: the four waves of a
+ * With Nq < Nk the fast modes run on a prefill kernel: the eight waves of a
  * workgroup split a 32-row tile's KV blocks into contiguous ranges of the
  * visit order; each range starts from the running maximum the row reached
  * before it, so the P codes are those of the sequential visit; only the FP32

@@ -4,7 +4,7 @@
 // and of a prefill kernel working on a KV cache.
 //
 // A tile of 32 query rows has only 32 rows of work per KV block, so one wave
-// would run the whole key sequence alone.  Here the four waves of a workgroup
+// would run the whole key sequence alone.  Here the eight waves of a workgroup
 // share the tile's KV blocks instead -- wave w takes a contiguous range of
 // the visit order -- without changing what Algorithm 1 computes:
 //   pass 1: each wave takes the row maxima of its blocks' scores; the
@@ -14,7 +14,7 @@
 //           running maximum, so every block sees exactly the running maximum
 //           of the sequential visit: P = exp2(fma(D, c, -mc)) and its E4M3
 //           code are those of the one-wave kernel (counts included);
-//   merge:  the four (O, l) partials are brought to the row's final maximum
+//   merge:  the eight (O, l) partials are brought to the row's final maximum
 //           (one exp2 each) and summed.  Only the FP32 rounding of O and l
 //           differs from the sequential chain of alpha products.
 // The scores are computed twice (once per pass); the second read of K comes
@@ -41,7 +41,7 @@ __device__ inline i32x2 read_tr8(const uint8_t* p)
     return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) i32x2*)(p));
 }
 
-constexpr int kPrefillWaves = 4;
+constexpr int kPrefillWaves = 8;
 
 }  // namespace
 
@@ -111,36 +111,49 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     }
 
     // ---- S^T = K_j Q^T, K fragments from HBM (key 32 kt + a_row_to_key(n)) ----
+    // The MFMAs of one 32-key tile wait on a single round of loads: all DK
+    // fragments of tile kt are requested together, one tile ahead (WHOLE: all
+    // tiles of the block at once, when the registers allow it), so a block
+    // costs KT / 2 .. 1 HBM round trips instead of DK.
     const int a_key = a_row_to_key(n);
     f32x16 s[KT];
-    auto qk = [&](int j) __attribute__((always_inline)) {
+    auto mfma_qk = [&](const QFrag& a, int kk, const f32x16& acc) __attribute__((always_inline)) {
+        if constexpr (QK8)
+            return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, qf[kk], acc, 0, 0, 0, 0, 0, 0);
+        else
+            return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
+    };
+    auto qk = [&](int j, auto whole) __attribute__((always_inline)) {
         const int t0 = j * BC;
-        const uint8_t* krow[KT];
+        auto load_tile = [&](QFrag* dst, int kt) __attribute__((always_inline)) {
+            const uint8_t* kr = Kg + (size_t)min(t0 + 32 * kt + a_key, Nk - 1) * KROW + (QSTEP / 2) * h;
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-            krow[kt] = Kg + (size_t)min(t0 + 32 * kt + a_key, Nk - 1) * KROW + (QSTEP / 2) * h;
-        auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
-            return *reinterpret_cast<const QFrag*>(krow[kt] + QSTEP * kk);
+            for (int kk = 0; kk < DK; ++kk)
+                dst[kk] = *reinterpret_cast<const QFrag*>(kr + QSTEP * kk);
         };
-        QFrag a[2][KT];
+        if constexpr (decltype(whole)::value) {
+            QFrag a[KT][DK];
 #pragma unroll
-        for (int kt = 0; kt < KT; ++kt)
-            a[0][kt] = kfrag(0, kt);
-#pragma unroll
-        for (int kk = 0; kk < DK; ++kk) {
-            if (kk + 1 < DK) {
-#pragma unroll
-                for (int kt = 0; kt < KT; ++kt)
-                    a[(kk + 1) & 1][kt] = kfrag(kk + 1, kt);
-            }
+            for (int kt = 0; kt < KT; ++kt)
+                load_tile(a[kt], kt);
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
-                const f32x16 acc = kk == 0 ? f32x16{} : s[kt];
-                if constexpr (QK8)
-                    s[kt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[kk & 1][kt], qf[kk], acc,
-                                                                            0, 0, 0, 0, 0, 0);
-                else
-                    s[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[kk & 1][kt], qf[kk], acc, 0, 0, 0);
+                s[kt] = mfma_qk(a[kt][0], 0, f32x16{});
+#pragma unroll
+                for (int kk = 1; kk < DK; ++kk)
+                    s[kt] = mfma_qk(a[kt][kk], kk, s[kt]);
+            }
+        } else {
+            QFrag a[2][DK];
+            load_tile(a[0], 0);
+#pragma unroll
+            for (int kt = 0; kt < KT; ++kt) {
+                if (kt + 1 < KT)
+                    load_tile(a[(kt + 1) & 1], kt + 1);
+                s[kt] = mfma_qk(a[kt & 1][0], 0, f32x16{});
+#pragma unroll
+                for (int kk = 1; kk < DK; ++kk)
+                    s[kt] = mfma_qk(a[kt & 1][kk], kk, s[kt]);
             }
         }
     };
@@ -172,7 +185,7 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     float m1 = -INFINITY;
     for (int it = it0; it < it1; ++it) {
         const int j = jof(it);
-        qk(j);
+        qk(j, std::true_type{});
         mask(j);
         m1 = fmax_f(m1, row_max());
     }
@@ -230,7 +243,7 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     for (int it = it0; it < it1; ++it) {
         const int j = jof(it);
         const int t0 = j * BC;
-        qk(j);
+        qk(j, std::false_type{});
         mask(j);
         const float mx = row_max();
         const bool vis = mx > -INFINITY;            // the row has a key in this block
