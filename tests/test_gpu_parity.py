@@ -37,7 +37,7 @@ def test_small_faithful_and_nocast(d, bkv, causal, order):
 def test_small_fast(d, bkv, causal, order):
     inp = make_inputs(2, 4, 2, 333, d, fmt="bf16_e4m3", delta=8.0, seed=200 + d + bkv)
     dev = to_device(inp)
-    for S in (1.0, 256.0, 448.0, 3.0, 512.0):
+    for S in (1.0, 256.0, 448.0, 3.0, 512.0, 0.0625, 1024.0):
         label = f"fast d={d} bkv={bkv} causal={causal} {order} S={S}"
         log(label)
         gpu = run_gpu(dev, "fast", S, order, causal, bkv)
@@ -154,20 +154,34 @@ def test_workload_sink_n1024_d64_faithful():
 
 
 def test_workload_sink_sweep_faithful():
+    """The Delta sweep: parity on sampled rows, and the report of this
+    workload -- the device's fraction of non-sink P cast to zero (all rows)
+    against F(Delta_eff, S) = Phi(Delta_eff + delta_4 - 10 ln 2 - ln S), and
+    the MSE against FP64 attention on the sampled rows."""
+    from oracle import analysis
+    import oracle
     w = WORKLOADS["sink_sweep_h8_n4096_d128_faithful"]
     base = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=0.0, seed=w.seed_base)
     rows = np.concatenate([np.arange(h * w.N, (h + 1) * w.N, 16) + (3 * h) % 16 for h in range(w.Hq)])
     rows = np.unique(np.concatenate([rows, np.arange(w.N - 130, w.N)]))
+    n_nonsink = w.B * w.Hq * w.N * (w.N - 4)
+    log("Delta_eff  S      order    zeroed non-sink   F(Delta,S)   MSE vs FP64")
     for D in (0.0, 5.0, 7.0, 9.0, 12.0):
         inp = with_delta(base, D)
         dev = to_device(inp)
+        ref, _ = oracle.ref_fp64(inp.q32, inp.k32, inp.v32, causal=w.causal, rows=rows)
         for S, order in itertools.product(w.scales, w.orders):
             label = f"{w.name} Delta={D} S={S} {order}"
-            log(label)
             gpu = run_gpu(dev, w.mode, S, order, w.causal, w.block_kv)
             compare(inp, gpu, w.mode, S, order, w.causal, w.block_kv, rows=rows, label=label)
+            frac = float(gpu[2][..., 1:].sum(dtype=np.uint64)) / n_nonsink
+            F = analysis.collapse_fraction(inp.delta_eff, S)
+            mse = float(np.mean((gpu[0].reshape(-1, w.d)[rows].astype(np.float64) - ref) ** 2))
+            log(f"{inp.delta_eff:8.4f}  {S:5.0f}  {order:8s} {frac:14.6f}   {F:10.6f}   {mse:.4e}")
+            if order == "forward":
+                assert abs(frac - F) <= 0.06, (label, frac, F)     # fixed point (d) on the device
             if order == "reverse" and S == 256.0:
-                assert gpu[2][..., 2].sum() == 0
+                assert gpu[2][..., 2].sum() == 0                    # fixed point (c) on the device
         del dev
         torch.cuda.empty_cache()
 
