@@ -49,6 +49,11 @@
  *                        through the *_descaled entry points.
  *   The E4M3 cast saturates: P*S >= 448 becomes 448 (reachable only for S > 448).
  *
+ * Alignment: q, k, v and out must be 16-byte aligned (the kernels move them in
+ * 16-byte vectors; rows of a contiguous tensor then stay aligned because
+ * d is 64 or 128), lse, counts and the diagnostic arrays 4-byte aligned;
+ * otherwise ATTN_ERR_INVALID_ARG.
+ *
  * Ownership and threading: every pointer is a device pointer owned by the
  * caller.  The library allocates no memory, keeps no per-call state, and is
  * reentrant.  Work is enqueued on `stream` (a hipStream_t; NULL = the null

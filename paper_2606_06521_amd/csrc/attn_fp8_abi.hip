@@ -76,6 +76,12 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     if (count ? !counts : !out)
         return ATTN_ERR_INVALID_ARG;
+    // the kernels move q, k, v and out in 16-byte vectors, lse and counts in
+    // 4-byte words (every row of a contiguous tensor then stays aligned)
+    auto misaligned = [](const void* ptr, uintptr_t a) { return ptr && ((uintptr_t)ptr % a) != 0; };
+    if (misaligned(q, 16) || misaligned(k, 16) || misaligned(v, 16) || misaligned(out, 16) ||
+        misaligned(lse, 4) || misaligned(counts, 4) || misaligned(gap_hist, 4) || misaligned(blk_zero, 4))
+        return ATTN_ERR_INVALID_ARG;
     if ((gap_hist || blk_zero) && (!count || !gap_hist || !blk_zero || nbins < 1 || nbins > 64))
         return ATTN_ERR_INVALID_ARG;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
@@ -245,7 +251,8 @@ const char* attn_fp8_strerror(int status)
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
                "and positive, Nq > Nk, or order/mode/causal/n_sink out of range; the dynamic scale "
                "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive; "
-               "the block diagnostic needs all three arrays and 1 <= nbins <= 64)";
+               "the block diagnostic needs all three arrays and 1 <= nbins <= 64; q, k, v and "
+               "out must be 16-byte aligned, lse and counts 4-byte aligned)";
     case ATTN_ERR_UNSUPPORTED:
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:

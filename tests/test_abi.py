@@ -163,3 +163,20 @@ def test_kv_entry_points_validate(A):
     cnt = A.attn_fp8_p_underflow_count_kv(FAKE, FAKE, FAKE, 1, 2, 1, 32, 4096, 128, 1, 128, 1,
                                           256.0, 1, 4, 1.0, 1.0, 1.0, None, None, None, None)
     assert cnt == -1
+
+
+def test_misaligned_pointers_are_rejected(A):
+    base = 1 << 20
+    def f(**kw):
+        a = dict(q=base, k=base, v=base, out=base, lse=None, mode=1)
+        a.update(kw)
+        return A.attn_fp8_fwd(a["q"], a["k"], a["v"], a["out"], a["lse"], 1, 2, 1, 64, 64, 0, 64, 0,
+                              256.0, a["mode"], None)
+    assert f(q=base + 8) == -1
+    assert f(k=base + 2) == -1
+    assert f(v=base + 1) == -1
+    assert f(out=base + 4) == -1
+    assert f(lse=base + 2) == -1
+    cnt = A.attn_fp8_p_underflow_count(base, base, base, 1, 2, 1, 64, 64, 0, 64, 0, 256.0, 1, 4,
+                                       base + 1, None, None, None)
+    assert cnt == -1
