@@ -42,6 +42,10 @@ KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast_kernel.hpp",
                   "paper_2606_06521_amd/csrc/attn_prefill.hip",
                   "paper_2606_06521_amd/csrc/attn_common.hpp"]
 HBM_PEAK_GBS = 8000.0
+# chip-wide v_exp_f32 rate measured by tests/test_gpu_probes.py::test_exp2_issue_rate
+# (16 independent chains per lane, all CUs): 1.83e13 exp2/s, i.e. one wave64
+# instruction per ~8.6 cycles per SIMD at 2.4 GHz
+EXP2_PEAK_PER_S = 1.83e13
 
 
 def traffic_file(workload: str) -> str:
@@ -266,6 +270,11 @@ def main() -> int:
             "mixed_bf16_fp8_peak": round(MIXED_PEAK, 1) if w.mode == "fast" else None,
             "frac_of_mixed_peak": round(achieved / MIXED_PEAK, 4) if w.mode == "fast" else None,
         },
+        # one exp2 per visible (row, key) pair, against the measured v_exp_f32 rate
+        "exp2": {"per_launch": w.pairs(),
+                 "achieved_per_s": float("%.4g" % (w.pairs() / (kernel_ms_avg * 1e-3))),
+                 "peak_per_s": EXP2_PEAK_PER_S,
+                 "frac": round(w.pairs() / (kernel_ms_avg * 1e-3) / EXP2_PEAK_PER_S, 4)},
         "p_underflow_counts": {"sink": counts_total[0], "sink_block_nonsink": counts_total[1],
                                "other_blocks": counts_total[2]},
         "input_gen_s": round(gen_s, 2),

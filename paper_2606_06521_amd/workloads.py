@@ -36,6 +36,16 @@ class Workload:
             return "e4m3"
         return "f32" if self.mode in ("faithful", "nocast") else "bf16_e4m3"
 
+    def pairs(self) -> int:
+        """Visible (query row, key) pairs per launch: one exp2, one P and one
+        E4M3 code each.  Row r of nq sits at key position N - nq + r."""
+        nq = self.rows
+        if not self.causal:
+            per_head = nq * self.N
+        else:
+            per_head = nq * (self.N - nq) + nq * (nq + 1) // 2
+        return self.B * self.Hq * per_head
+
     def flops(self) -> float:
         """FlashAttention convention: 4*B*Hq*N^2*d, halved under causal masking.
         With nq query rows against N cached keys: 4 d per (row, visible key)."""

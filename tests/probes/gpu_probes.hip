@@ -6,7 +6,9 @@
 //   - v_exp_f32 (exp2 in the fast kernels),
 //   - the operand/accumulator lane layouts of the three MFMA shapes used,
 //   - the per-lane E8M0 operand scales of the block-scaled FP8 MFMA and the
-//     per-lane scale of the scaled convert (the dynamic P-scale).
+//     per-lane scale of the scaled convert (the dynamic P-scale),
+//   - the chip-wide issue rate of v_exp_f32 (the exp2 peak the attention
+//     kernels are measured against).
 // Every kernel bounds-checks its index against n.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -58,6 +60,27 @@ __global__ void k_exp2(const float* x, int64_t n, float* out)
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i < n)
         out[i] = __builtin_amdgcn_exp2f(x[i]);
+}
+
+// v_exp_f32 throughput: every lane runs 16 independent chains x <- exp2(-x)
+// (which stays in [0.5, 1]) for `iters` rounds; 256-thread workgroups, one
+// result per lane written so the work is kept.
+__global__ void __launch_bounds__(256) k_exp2_rate(int iters, float* out)
+{
+    float x[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        x[i] = 0.5f + 0.03125f * (float)i + 1e-6f * (float)threadIdx.x;
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            x[i] = __builtin_amdgcn_exp2f(-x[i]);
+    }
+    float acc = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+        acc += x[i];
+    out[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc;
 }
 
 // One wave.  A: 32x16 bf16 (row-major), B: 16x32 bf16, D: 32x32 f32.
@@ -209,6 +232,15 @@ int probe_cvt_scaled_vec(const float* x, const float* scale, int64_t n, uint8_t*
         return -1;
     hipLaunchKernelGGL(k_cvt_scaled_vec, dim3(grid_for(n / 2, 256)), dim3(256), 0, (hipStream_t)stream,
                        x, scale, n, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// `out` holds blocks * 256 floats; exp2 evaluations = blocks * 256 * iters * 16
+int probe_exp2_rate(int blocks, int iters, float* out, void* stream)
+{
+    if (blocks <= 0 || iters <= 0 || !out)
+        return -1;
+    hipLaunchKernelGGL(k_exp2_rate, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters, out);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

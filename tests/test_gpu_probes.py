@@ -114,6 +114,33 @@ def test_exp2_accuracy(probes):
     assert err.max() <= 2.0, err.max()
 
 
+def test_exp2_issue_rate(probes):
+    """Chip-wide v_exp_f32 rate, the exp2 peak the benchmark reports the
+    attention kernels against: 2048 workgroups x 256 lanes x 16 independent
+    chains x 4096 rounds, timed with events on the launch stream (median of
+    five launches).  The results must be finite and each lane's sum of its 16
+    chains in [8, 16]."""
+    blocks, iters, chains = 2048, 4096, 16
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    assert probes.probe_exp2_rate(blocks, 64, out.data_ptr(), s.cuda_stream) == 0   # warm-up
+    times = []
+    for _ in range(5):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s)
+        assert probes.probe_exp2_rate(blocks, iters, out.data_ptr(), s.cuda_stream) == 0
+        e1.record(s)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1) / 1e3)
+    sec = float(np.median(times))
+    rate = blocks * 256 * iters * chains / sec
+    y = out.cpu().numpy()
+    assert np.all(np.isfinite(y)) and y.min() >= 8.0 and y.max() <= 16.0
+    print(f"v_exp_f32 issue rate: {rate:.4e} exp2/s ({sec * 1e3:.3f} ms per launch)", flush=True)
+    # between 1/64 and 1 evaluation per lane per cycle at 2.4 GHz on 256 CUs
+    assert 256 * 256 * 2.4e9 / 64 < rate < 256 * 256 * 2.4e9
+
+
 def test_mfma_bf16_layout(probes):
     rng = np.random.default_rng(8)
     A = rng.integers(-8, 9, (32, 16)).astype(np.float32)

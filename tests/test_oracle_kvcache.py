@@ -64,3 +64,15 @@ def test_rejects_more_queries_than_keys():
     q = np.concatenate([full.q32, full.q32], axis=2)
     with pytest.raises(ValueError):
         oracle.attn(q, full.k32, full.v32, S=256.0, order="forward", block_kv=64)
+
+
+@pytest.mark.parametrize("nq,nk,causal", [(5, 5, True), (3, 17, True), (7, 7, False), (4, 9, False), (1, 1, True)])
+def test_workload_pair_count_is_the_visible_pairs(nq, nk, causal):
+    """Workload.pairs() (the exp2 count the benchmark reports) equals a brute
+    count of the (row, key) pairs the mask leaves visible, with row r of nq at
+    key position nk - nq + r."""
+    from paper_2606_06521_amd.workloads import Workload
+    w = Workload("t", 2, 3, 3, nk, 64, causal, "fast", 64, (0.0,), (256.0,), ("reverse",),
+                 nq=nq if nq < nk else 0)
+    brute = sum(1 for r in range(nq) for t in range(nk) if not causal or t <= nk - nq + r)
+    assert w.pairs() == 2 * 3 * brute
