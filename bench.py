@@ -91,18 +91,30 @@ def parse():
 
 
 def write_traffic(fetch_csv: str, write_csv: str, workload: str, copy_mib: int = 1024) -> dict:
-    """HBM bytes per launch of the fast kernel from the two counter passes.
+    """HBM bytes per call of the attention path from the two counter passes.
     Each counter is scaled by bytes_copied / counter_reading of the largest
-    device copy in the same run (a plain copy of ``copy_mib`` MiB)."""
+    device copy in the same run (a plain copy of ``copy_mib`` MiB).  A call is
+    one kernel, or for a split prefill its three launches (range maxima,
+    pass 2, merge): the average of each kind of launch is summed."""
     import csv
 
     def read(path):
         rows = list(csv.DictReader(open(path)))
-        # the timed launches: causal, no counts, static power-of-two scale
-        kern = [float(r["Counter_Value"]) for r in rows if "_kernel<" in r["Kernel_Name"]
-                and ", true, false, 1," in r["Kernel_Name"]]
+        name = lambda r: r["Kernel_Name"]
+        kinds = [
+            # the timed launches: causal, no counts, static power-of-two scale
+            lambda r: "_kernel<" in name(r) and ", true, false, 1," in name(r),
+            # a split prefill's range-maxima launch and its merge
+            lambda r: "prefill_kernel<" in name(r) and name(r).split("(")[0].endswith(", 1>"),
+            lambda r: "prefill_merge<" in name(r),
+        ]
+        per_call = 0.0
+        for k in kinds:
+            vals = [float(r["Counter_Value"]) for r in rows if k(r)]
+            if vals:
+                per_call += sum(vals) / len(vals)
         copy = max(float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"])
-        return sum(kern) / len(kern), copy
+        return per_call, copy
 
     f_kib, f_copy = read(fetch_csv)
     w_kib, w_copy = read(write_csv)

@@ -55,8 +55,11 @@
  * otherwise ATTN_ERR_INVALID_ARG.
  *
  * Ownership and threading: every pointer is a device pointer owned by the
- * caller.  The library allocates no memory, keeps no per-call state, and is
- * reentrant.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ * caller.  The library keeps no per-call state and is reentrant.  It
+ * allocates no memory, except that a KV-cache call whose 32-row tiles cannot
+ * fill the GPU takes a temporary workspace (see attn_fp8_fwd_kv): a
+ * stream-ordered allocation on `stream`, released the same way before the
+ * call returns, so it never outlives the work enqueued by that call.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
  * stream) and runs asynchronously: a return of ATTN_OK means "validated and
  * launched"; synchronise on the stream before reading results.
  *
@@ -195,8 +198,15 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
  * workgroup split a 32-row tile's KV blocks into contiguous ranges of the
  * visit order; each range starts from the running maximum the row reached
  * before it, so the P codes are those of the sequential visit; only the FP32
- * summation order of O and l differs.  Nq > Nk returns ATTN_ERR_INVALID_ARG;
- * other arguments and return codes as for the descaled entry points.
+ * summation order of O and l differs.  (Long chunks, Nq >= 128 with Nk - Nq a
+ * multiple of block_kv, run on the square problem's kernel instead.)  When
+ * the tiles are fewer than the GPU's compute units, each tile is split over
+ * C = min(CUs / tiles, blocks / 8, 8) workgroups and the call enqueues three
+ * kernels (the range maxima, Algorithm 1 per range, a merge) with a
+ * workspace of tiles * C * (8 * 32 + 32 * d + 32) floats taken from a
+ * stream-ordered allocation; if that allocation fails the tiles run unsplit
+ * (same results).  Nq > Nk returns ATTN_ERR_INVALID_ARG; other arguments and
+ * return codes as for the descaled entry points.
  */
 int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse,
                     int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,

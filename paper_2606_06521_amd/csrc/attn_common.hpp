@@ -59,6 +59,11 @@ struct Params {
     // tiles (t, n_tiles - 1 - t) of one (batch, head)
     int pairs;           // units per (batch, head) = ceil(n_tiles / 2)
     long long units;     // B * Hq * pairs
+    // prefill kernel split over several workgroups per 32-row tile (nsplit
+    // > 1); the workspace is owned by the launcher for the duration of a call
+    int nsplit;          // workgroups per tile (1: one fused workgroup)
+    float* ws_max;       // [tile][nsplit * waves][32] row maxima of each wave range
+    float* ws_part;      // [tile][nsplit][32 * d + 32] each workgroup's O sum, then l
 };
 
 // how the fast kernel applies the P-scale

@@ -1,6 +1,8 @@
 // C ABI of libattn_fp8.so (declared in include/attn_fp8.h): argument
 // validation, choice of kernel instantiation, grid sizing, launch on the
-// caller's stream.  No memory is allocated and no state is kept.
+// caller's stream.  No state is kept; the only memory taken is the prefill
+// kernel's split workspace, allocated and released in stream order on the
+// caller's stream within the call.
 #include "../../include/attn_fp8.h"
 #include "attn_common.hpp"
 #include "attn_launch.hpp"
@@ -10,7 +12,7 @@
 
 namespace {
 
-constexpr int kVersion = 500;   // 0.5.0: KV-cache prefill shape (Nq queries, Nk keys)
+constexpr int kVersion = 510;   // 0.5.1: KV-cache prefill tiles split over workgroups
 
 // Clears the diagnostic's output arrays on the caller's stream (a kernel, not
 // a memset node, so the call stays safe inside a captured graph).
@@ -131,8 +133,16 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.pairs = (int)((n_tiles + 1) / 2);
     p.units = (long long)B * Hq * p.pairs;
 
+    p.nsplit = 1;
+    p.ws_max = nullptr;
+    p.ws_part = nullptr;
+
     hipStream_t s = static_cast<hipStream_t>(stream);
     hipError_t e;
+    int dev = 0, n_cu = 0;
+    if (fast && (hipGetDevice(&dev) != hipSuccess ||
+                 hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess))
+        return ATTN_ERR_HIP;
     if (gap_hist) {
         const int64_t nz = (int64_t)B * Hq * p.nblk_all;
         hipLaunchKernelGGL(zero_u32, dim3(1024), dim3(256), 0, s, gap_hist, nz * nbins);
@@ -144,7 +154,7 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
         const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
         e = attn::launch_prefill(p, d, block_kv, causal != 0, count, scale,
-                                 mode == ATTN_MODE_FP8QK, s);
+                                 mode == ATTN_MODE_FP8QK, n_cu, s);
     } else if (fast) {
         // the scaled convert applies 1/S exactly only for S = 2^k, and only
         // below the E4M3 range limit (it does not saturate)
@@ -152,10 +162,6 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
         // persistent grid: one workgroup per CU (the LDS footprint admits no
         // second one), 8 XCDs, never more workgroups than work units
-        int dev = 0, n_cu = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return ATTN_ERR_HIP;
         const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
         const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
                                                                             : per_xcd_max;

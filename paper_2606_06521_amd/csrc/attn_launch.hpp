@@ -19,9 +19,11 @@ hipError_t launch_fast_qk8(const Params& p, int grid, int d, int block_kv, bool 
 int fast_rows_per_wg(int d, int block_kv);
 
 // queries against a longer KV cache (p.Nk > p.N), fast modes: one workgroup
-// per (batch, head, 32-row query tile), grid p.per_xcd * 8
+// per (batch, head, 32-row query tile), or several per tile when the tiles
+// cannot fill n_cu compute units (two launches and a temporary workspace on
+// the stream); sets its own grid, nsplit and workspace fields of p
 hipError_t launch_prefill(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
-                          bool qk8, hipStream_t stream);
+                          bool qk8, int n_cu, hipStream_t stream);
 int prefill_rows_per_wg();
 
 }  // namespace attn

@@ -20,6 +20,19 @@
 // The scores are computed twice (once per pass); the second read of K comes
 // from L2.
 //
+// When the tiles alone cannot fill the chip, each tile is split over nsplit
+// workgroups (the visit order cut into nsplit * 8 contiguous wave ranges) and
+// the passes become two launches:
+//   PHASE 1: every wave writes the row maxima of its range to the workspace;
+//   PHASE 2: every wave starts from the maximum over all earlier ranges (read
+//            back from the workspace), runs Algorithm 1 over its range, and
+//            brings its (O, l) to the tile's final maximum; each workgroup
+//            writes the sum of its eight waves to the workspace;
+//   merge:   a third launch (prefill_merge) adds the nsplit partial sums of
+//            each tile in a fixed order and writes out and lse.  The launch
+//            boundaries order the phases; no workgroup waits on another.
+// PHASE 0 is the one-workgroup kernel with both passes fused.
+//
 // K fragments (the S^T MFMA's A operand) are read straight from HBM, 16
 // bytes per lane, in the key order of a_row_to_key.  Each wave stages the V
 // block it multiplies in its own LDS region, in the XOR-swizzled layout read
@@ -41,11 +54,25 @@ __device__ inline i32x2 read_tr8(const uint8_t* p)
     return __builtin_amdgcn_ds_read_tr8_b64_v2i32((__attribute__((address_space(3))) i32x2*)(p));
 }
 
+// One 16-byte-per-lane direct load: lane i reads HBM bytes [base + voff, +16)
+// and writes LDS bytes [dst + 16 i, +16).  Inline assembly, so that its
+// completion is awaited only where the kernel says (s_waitcnt vmcnt(0) before
+// the LDS stage is read).  M0 carries the LDS base and is used by nothing
+// else in this kernel.
+__device__ inline void g2lds(const uint8_t* base, uint32_t voff, const uint8_t* dst)
+{
+    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)dst;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(base)
+                 : "memory");
+}
+
 constexpr int kPrefillWaves = 8;
 
 }  // namespace
 
-template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8>
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8, int PHASE>
 __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
 {
     constexpr int NW = kPrefillWaves;
@@ -69,9 +96,24 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     __shared__ float lsh[NW][32];     // merge: each wave's l, at the final maximum
     __shared__ uint32_t csh[32][3];   // merge: counts
 
-    int bh, tile;
-    if (!map_tile<false>(p, bh, tile))
-        return;
+    // workgroup -> (tile unit, part cidx of C); the C workgroups of a unit are
+    // consecutive logical indices inside one XCD's contiguous range
+    // (per_xcd is a multiple of C), so they share that XCD's L2
+    const int C = PHASE == 0 ? 1 : p.nsplit;
+    int unit, cidx;
+    {
+        const int i = blockIdx.x;
+        const int slot = i / kNumXcd;
+        if (slot >= p.per_xcd)
+            return;
+        const int L = (i % kNumXcd) * p.per_xcd + slot;
+        if (L >= p.total_wg)
+            return;
+        unit = L / C;
+        cidx = L - unit * C;
+    }
+    const int bh = unit / p.n_tiles;
+    const int tile = unit - bh * p.n_tiles;
     const int Nq = p.N, Nk = p.Nk, qoff = p.qoff;
     const int b = bh / p.Hq;
     const int hq = bh - b * p.Hq;
@@ -84,9 +126,12 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     const int row = 32 * tile + n;              // every wave holds the same 32 rows
     const int pos = row + qoff;                 // the row's key position
     const int rlast = min(32 * tile + 31, Nq - 1);
-    // blocks the tile visits, and this wave's contiguous range of the visit order
+    // blocks the tile visits, and this wave's contiguous range g of the visit
+    // order (C * NW ranges, part cidx holding ranges cidx NW .. cidx NW + NW - 1)
     const int nbt = CAUSAL ? (rlast + qoff) / BC + 1 : (Nk + BC - 1) / BC;
-    const int it0 = nbt * w / NW, it1 = nbt * (w + 1) / NW;
+    const int R = C * NW;
+    const int g = cidx * NW + w;
+    const int it0 = nbt * g / R, it1 = nbt * (g + 1) / R;
     auto jof = [&](int it) __attribute__((always_inline)) { return p.order == 0 ? it : nbt - 1 - it; };
 
     const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * Nq * KROW;
@@ -182,22 +227,45 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     };
 
     // ---- pass 1: row maxima over this wave's blocks ----
-    float m1 = -INFINITY;
-    for (int it = it0; it < it1; ++it) {
-        const int j = jof(it);
-        qk(j, std::true_type{});
-        mask(j);
-        m1 = fmax_f(m1, row_max());
-    }
-    if (h == 0)
-        tab[w][n] = m1;
-    __syncthreads();
     float m_start = -INFINITY, m_final = -INFINITY;
+    if constexpr (PHASE != 2) {
+        float m1 = -INFINITY;
+        for (int it = it0; it < it1; ++it) {
+            const int j = jof(it);
+            qk(j, std::true_type{});
+            mask(j);
+            m1 = fmax_f(m1, row_max());
+        }
+        if constexpr (PHASE == 1) {
+            if (h == 0)
+                p.ws_max[((size_t)unit * R + g) * 32 + n] = m1;
+            return;
+        }
+        if (h == 0)
+            tab[w][n] = m1;
+        __syncthreads();
 #pragma unroll
-    for (int v = 0; v < NW; ++v) {
-        if (v < w)
-            m_start = fmax_f(m_start, tab[v][n]);
-        m_final = fmax_f(m_final, tab[v][n]);
+        for (int v = 0; v < NW; ++v) {
+            if (v < w)
+                m_start = fmax_f(m_start, tab[v][n]);
+            m_final = fmax_f(m_final, tab[v][n]);
+        }
+    } else {
+        // the maxima of every range of the tile, from the PHASE 1 launch, read
+        // eight ranges (one part) per round
+        const float* mx = p.ws_max + (size_t)unit * R * 32 + n;
+        for (int cc = 0; cc < C; ++cc) {
+            float t[NW];
+#pragma unroll
+            for (int v = 0; v < NW; ++v)
+                t[v] = mx[32 * (cc * NW + v)];
+#pragma unroll
+            for (int v = 0; v < NW; ++v) {
+                if (cc * NW + v < g)
+                    m_start = fmax_f(m_start, t[v]);
+                m_final = fmax_f(m_final, t[v]);
+            }
+        }
     }
 
     // ---- pass 2: Algorithm 1 over this wave's range, from the running maximum m_start ----
@@ -222,27 +290,26 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     const int j16 = n & 15;
     const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
                                        8 * (j16 & 1));
-    // V_j -> this wave's LDS stage: round i writes LDS bytes [1024 i, +1024);
-    // lane l fills row i V_RPI + l / VCPR at physical chunk l % VCPR, which
-    // holds logical chunk (l % VCPR) ^ vswz(row)
-    auto stage_v = [&](int j) __attribute__((always_inline)) {
+    // V_j -> this wave's LDS stage, straight from HBM: round i writes LDS bytes
+    // [1024 i, +1024); lane l fills row i V_RPI + l / VCPR at physical chunk
+    // l % VCPR, which holds logical chunk (l % VCPR) ^ vswz(row).  Issued at
+    // the start of the block, so it travels with the K loads of the scores;
+    // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
+    // Nk - 1; their P is 0.
+    auto issue_v = [&](int j) __attribute__((always_inline)) {
         const int t0 = j * BC;
-        i32x4 tmp[V_NI];
 #pragma unroll
         for (int i = 0; i < V_NI; ++i) {
             const int rv = i * V_RPI + lane / VCPR;
             const int lc = (lane % VCPR) ^ vswz(rv);
-            tmp[i] = *reinterpret_cast<const i32x4*>(Vg + (size_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc);
+            g2lds(Vg, (uint32_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc, vst + 1024 * i);
         }
-#pragma unroll
-        for (int i = 0; i < V_NI; ++i)
-            *reinterpret_cast<i32x4*>(vst + 1024 * i + 16 * lane) = tmp[i];
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     };
 
     for (int it = it0; it < it1; ++it) {
         const int j = jof(it);
         const int t0 = j * BC;
+        issue_v(j);
         qk(j, std::false_type{});
         mask(j);
         const float mx = row_max();
@@ -324,7 +391,7 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
         mc_run = mc_new;
 
         // O^T += V_j^T P8^T
-        stage_v(j);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 #pragma unroll
         for (int i = 0; i < PVS * DT; ++i) {
             const int js = i / DT, dt = i % DT;
@@ -379,6 +446,38 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     }
     __syncthreads();
     const float* mb = reinterpret_cast<const float*>(lds);
+    if constexpr (PHASE == 2) {
+        // this workgroup's sum over its waves (at the tile's final maximum)
+        constexpr int PART = 32 * D + 32;
+        float* part = p.ws_part + ((size_t)unit * C + cidx) * PART;
+        for (int e = tid; e < 32 * D / 4; e += 64 * NW) {
+            f32x4 acc = *reinterpret_cast<const f32x4*>(mb + 4 * e);
+#pragma unroll
+            for (int v = 1; v < NW; ++v) {
+                const f32x4 t = *reinterpret_cast<const f32x4*>(mb + v * 32 * D + 4 * e);
+                acc[0] += t[0];
+                acc[1] += t[1];
+                acc[2] += t[2];
+                acc[3] += t[3];
+            }
+            *reinterpret_cast<f32x4*>(part + 4 * e) = acc;
+        }
+        if (tid < 32) {
+            float l = 0.f;
+#pragma unroll
+            for (int v = 0; v < NW; ++v)
+                l += lsh[v][tid];
+            part[32 * D + tid] = l;
+            if (COUNT && 32 * tile + tid < Nq) {
+                // the host clears the counts before a split launch
+                const size_t flat = (size_t)bh * Nq + 32 * tile + tid;
+                atomicAdd(p.counts + 3 * flat + 0, csh[tid][0]);
+                atomicAdd(p.counts + 3 * flat + 1, csh[tid][1]);
+                atomicAdd(p.counts + 3 * flat + 2, csh[tid][2]);
+            }
+        }
+        return;
+    }
     for (int e = tid; e < 32 * D / 4; e += 64 * NW) {
         const int rr = e / (D / 4);
         const int grow = 32 * tile + rr;
@@ -414,13 +513,8 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
 #pragma unroll
         for (int v = 0; v < NW; ++v)
             l += lsh[v][tid];
-        if (p.lse) {
-            float mf = -INFINITY;
-#pragma unroll
-            for (int v = 0; v < NW; ++v)
-                mf = fmax_f(mf, tab[v][tid]);
-            p.lse[flat] = (mf * c + __builtin_log2f(l)) * 0.6931471805599453f;
-        }
+        if (p.lse)   // lane tid of wave 0 holds row tid: m_final is that row's maximum
+            p.lse[flat] = (m_final * c + __builtin_log2f(l)) * 0.6931471805599453f;
         if (COUNT) {
             p.counts[3 * flat + 0] = csh[tid][0];
             p.counts[3 * flat + 1] = csh[tid][1];
@@ -429,51 +523,216 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     }
 }
 
+// Merge of a split tile: workgroup (tile, g) of 128 threads takes rows
+// 4 g .. 4 g + 3 of the tile, one 16-byte piece of a row per thread; the
+// nsplit partial sums are added in a fixed order and divided by S l.  lse
+// comes from the tile's final row maxima (the largest of its range maxima).
+template <int D>
+__global__ void __launch_bounds__(128) prefill_merge(Params p)
+{
+    constexpr int PART = 32 * D + 32;
+    constexpr int PIECES = D / 4;               // 16-byte pieces per row
+    const int unit = blockIdx.x / 8;
+    const int rg = blockIdx.x % 8;
+    if (unit >= p.total_wg / p.nsplit)
+        return;
+    const int C = p.nsplit;
+    const int bh = unit / p.n_tiles;
+    const int tile = unit - bh * p.n_tiles;
+    const int Nq = p.N;
+    const int t = threadIdx.x;
+    if (t >= 4 * PIECES)
+        return;
+    const int rr = 4 * rg + t / PIECES;           // row in the tile
+    const int piece = t % PIECES;
+    const int grow = 32 * tile + rr;
+    if (grow >= Nq)
+        return;
+    const float* base = p.ws_part + (size_t)unit * C * PART;
+    f32x4 part[8];
+    float lp[8];
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) {
+        if (cc < C) {
+            part[cc] = *reinterpret_cast<const f32x4*>(base + cc * PART + rr * D + 4 * piece);
+            lp[cc] = base[cc * PART + 32 * D + rr];
+        }
+    }
+    f32x4 acc = part[0];
+    float l = lp[0];
+#pragma unroll
+    for (int cc = 1; cc < 8; ++cc) {
+        if (cc < C) {
+            acc[0] += part[cc][0];
+            acc[1] += part[cc][1];
+            acc[2] += part[cc][2];
+            acc[3] += part[cc][3];
+            l += lp[cc];
+        }
+    }
+    const size_t flat = (size_t)bh * Nq + grow;
+    if (p.out) {
+        const float inv = p.v_descale / (p.S * l);
+        f32x4 v4;
+        v4[0] = acc[0] * inv;
+        v4[1] = acc[1] * inv;
+        v4[2] = acc[2] * inv;
+        v4[3] = acc[3] * inv;
+        *reinterpret_cast<f32x4*>(p.out + flat * D + 4 * piece) = v4;
+    }
+    if (piece == 0 && p.lse) {
+        constexpr int NW = kPrefillWaves;
+        float mf = -INFINITY;
+        const float* mx = p.ws_max + (size_t)unit * C * NW * 32 + rr;
+        for (int cc = 0; cc < C; ++cc) {
+            float t[NW];
+#pragma unroll
+            for (int v = 0; v < NW; ++v)
+                t[v] = mx[32 * (cc * NW + v)];
+#pragma unroll
+            for (int v = 0; v < NW; ++v)
+                mf = fmax_f(mf, t[v]);
+        }
+        p.lse[flat] = (mf * p.c + __builtin_log2f(l)) * 0.6931471805599453f;
+    }
+}
+
 namespace {
 
-template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE>
+// Clears the counts a split launch adds to.
+__global__ void prefill_zero(uint32_t* a, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        a[i] = 0u;
+}
+
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, int PHASE>
 hipError_t launch_one(const Params& p, bool qk8, hipStream_t s)
 {
     const int grid = p.per_xcd * kNumXcd;
     if (qk8)
-        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, true>), dim3(grid),
+        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, true, PHASE>), dim3(grid),
                            dim3(64 * kPrefillWaves), 0, s, p);
     else
-        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, false>), dim3(grid),
+        hipLaunchKernelGGL((prefill_kernel<D, BC, CAUSAL, COUNT, SCALE, false, PHASE>), dim3(grid),
                            dim3(64 * kPrefillWaves), 0, s, p);
     return hipGetLastError();
 }
 
+// PHASE 1 computes only maxima: one instantiation per shape, whatever the
+// scale and diagnostics
 template <int D, int BC, bool CAUSAL, bool COUNT>
-hipError_t launch_scale(const Params& p, int scale, bool qk8, hipStream_t s)
+hipError_t launch_scale(const Params& p, int scale, bool qk8, int phase, hipStream_t s)
 {
+    if (phase == 1)
+        return launch_one<D, BC, CAUSAL, false, kScaleAny, 1>(p, qk8, s);
+    if (phase == 2) {
+        if (scale == kScaleDynamic)
+            return launch_one<D, BC, CAUSAL, COUNT, kScaleDynamic, 2>(p, qk8, s);
+        if (scale == kScalePow2)
+            return launch_one<D, BC, CAUSAL, COUNT, kScalePow2, 2>(p, qk8, s);
+        return launch_one<D, BC, CAUSAL, COUNT, kScaleAny, 2>(p, qk8, s);
+    }
     if (scale == kScaleDynamic)
-        return launch_one<D, BC, CAUSAL, COUNT, kScaleDynamic>(p, qk8, s);
+        return launch_one<D, BC, CAUSAL, COUNT, kScaleDynamic, 0>(p, qk8, s);
     if (scale == kScalePow2)
-        return launch_one<D, BC, CAUSAL, COUNT, kScalePow2>(p, qk8, s);
-    return launch_one<D, BC, CAUSAL, COUNT, kScaleAny>(p, qk8, s);
+        return launch_one<D, BC, CAUSAL, COUNT, kScalePow2, 0>(p, qk8, s);
+    return launch_one<D, BC, CAUSAL, COUNT, kScaleAny, 0>(p, qk8, s);
 }
 
 template <int D, int BC>
-hipError_t launch_d_bc(const Params& p, bool causal, bool count, int scale, bool qk8, hipStream_t s)
+hipError_t launch_d_bc(const Params& p, bool causal, bool count, int scale, bool qk8, int phase,
+                       hipStream_t s)
 {
     if (causal)
-        return count ? launch_scale<D, BC, true, true>(p, scale, qk8, s)
-                     : launch_scale<D, BC, true, false>(p, scale, qk8, s);
-    return count ? launch_scale<D, BC, false, true>(p, scale, qk8, s)
-                 : launch_scale<D, BC, false, false>(p, scale, qk8, s);
+        return count ? launch_scale<D, BC, true, true>(p, scale, qk8, phase, s)
+                     : launch_scale<D, BC, true, false>(p, scale, qk8, phase, s);
+    return count ? launch_scale<D, BC, false, true>(p, scale, qk8, phase, s)
+                 : launch_scale<D, BC, false, false>(p, scale, qk8, phase, s);
 }
+
+hipError_t launch_phase(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
+                        bool qk8, int phase, hipStream_t stream)
+{
+    if (d == 64)
+        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, scale, qk8, phase, stream)
+                              : launch_d_bc<64, 128>(p, causal, count, scale, qk8, phase, stream);
+    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, scale, qk8, phase, stream)
+                          : launch_d_bc<128, 128>(p, causal, count, scale, qk8, phase, stream);
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-hipError_t launch_prefill(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
-                          bool qk8, hipStream_t stream)
+// Tiles (32 query rows of one batch and head) that cannot fill the chip are
+// split over C workgroups each: C = min(n_cu / tiles, blocks / 8, 8), so that
+// every wave range holds at least one KV block.  The split needs a workspace
+// (range maxima, per-workgroup partial sums), taken with a stream-ordered
+// allocation on the caller's stream and released the same way after the
+// three launches; if that allocation fails the tile runs unsplit.
+hipError_t launch_prefill(const Params& p_in, int d, int block_kv, bool causal, bool count, int scale,
+                          bool qk8, int n_cu, hipStream_t stream)
 {
-    if (d == 64)
-        return block_kv == 64 ? launch_d_bc<64, 64>(p, causal, count, scale, qk8, stream)
-                              : launch_d_bc<64, 128>(p, causal, count, scale, qk8, stream);
-    return block_kv == 64 ? launch_d_bc<128, 64>(p, causal, count, scale, qk8, stream)
-                          : launch_d_bc<128, 128>(p, causal, count, scale, qk8, stream);
+    Params p = p_in;
+    p.nsplit = 1;
+    p.ws_max = nullptr;
+    p.ws_part = nullptr;
+    const long long units = (long long)p.B * p.Hq * p.n_tiles;
+    // blocks the last tile visits (no tile visits more)
+    const long long nb_max = causal ? ((long long)p.N - 1 + p.qoff) / block_kv + 1
+                                    : ((long long)p.Nk + block_kv - 1) / block_kv;
+    long long C = 1;
+    if (units < n_cu) {
+        C = n_cu / units;
+        if (C > nb_max / kPrefillWaves)
+            C = nb_max / kPrefillWaves;
+        if (C > 8)
+            C = 8;
+        if (C < 1)
+            C = 1;
+    }
+    void* ws = nullptr;
+    size_t off_part = 0;
+    if (C > 1) {
+        const size_t n_max = (size_t)units * C * kPrefillWaves * 32;
+        const size_t n_part = (size_t)units * C * (32 * (size_t)d + 32);
+        off_part = align256(n_max * sizeof(float));
+        const size_t bytes = off_part + align256(n_part * sizeof(float));
+        if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) {
+            (void)hipGetLastError();
+            ws = nullptr;
+            C = 1;
+        }
+    }
+    if (C == 1) {
+        p.total_wg = (int)units;
+        p.per_xcd = (int)((units + kNumXcd - 1) / kNumXcd);
+        return launch_phase(p, d, block_kv, causal, count, scale, qk8, 0, stream);
+    }
+    p.nsplit = (int)C;
+    p.total_wg = (int)(units * C);
+    p.per_xcd = (int)((units + kNumXcd - 1) / kNumXcd * C);
+    p.ws_max = static_cast<float*>(ws);
+    p.ws_part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + off_part);
+    if (count)
+        hipLaunchKernelGGL(prefill_zero, dim3(1024), dim3(256), 0, stream, p.counts,
+                           (int64_t)p.B * p.Hq * p.N * 3);
+    hipError_t e = hipGetLastError();
+    if (e == hipSuccess)
+        e = launch_phase(p, d, block_kv, causal, count, scale, qk8, 1, stream);
+    if (e == hipSuccess)
+        e = launch_phase(p, d, block_kv, causal, count, scale, qk8, 2, stream);
+    if (e == hipSuccess) {
+        if (d == 64)
+            hipLaunchKernelGGL(prefill_merge<64>, dim3((unsigned)(units * 8)), dim3(128), 0, stream, p);
+        else
+            hipLaunchKernelGGL(prefill_merge<128>, dim3((unsigned)(units * 8)), dim3(128), 0, stream, p);
+        e = hipGetLastError();
+    }
+    const hipError_t ef = hipFreeAsync(ws, stream);
+    return e != hipSuccess ? e : ef;
 }
 
 int prefill_rows_per_wg() { return 32; }

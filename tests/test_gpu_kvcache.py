@@ -51,6 +51,26 @@ def test_long_chunks(mode, bkv):
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
+@pytest.mark.parametrize("mode", ["fast", "fp8qk"])
+@pytest.mark.parametrize("d,bkv,nk", [(128, 128, 2000), (64, 64, 4500), (128, 64, 1100), (64, 128, 3000)])
+def test_split_over_workgroups(mode, d, bkv, nk):
+    # Few 32-row tiles against many KV blocks: the prefill kernel splits each
+    # tile's visit order over C = min(CUs / tiles, blocks / 8, 8) workgroups
+    # (on 256 CUs: C = 2, 8, 2 and 3 for these caches), two launches and a
+    # cross-workgroup merge.  Ragged caches, one row and a ragged 45-row chunk.
+    full = make_inputs(1, 2, 1, nk, d, fmt=FMT[mode], delta=9.0, seed=970 + d + bkv + nk)
+    for nq in (1, 45):
+        inp = last_queries(full, nq)
+        dev = to_device(inp)
+        for (causal, order), (S, scale) in itertools.product(
+                itertools.product([False, True], ["forward", "reverse"]),
+                [(256.0, "static"), (448.0, "static"), (16.0, "dynamic")]):
+            label = f"kv split {mode} nq={nq} nk={nk} d={d} bkv={bkv} causal={causal} {order} S={S} {scale}"
+            log(label)
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale=scale)
+            compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
+
+
 def test_nocast_and_descales():
     full = make_inputs(1, 2, 1, 300, 128, fmt="f32", delta=7.0, seed=950)
     inp = last_queries(full, 40)
