@@ -71,6 +71,19 @@ def test_split_over_workgroups(mode, d, bkv, nk):
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
+def test_split_over_workgroups_descaled():
+    # a split tile (C = 4) with per-tensor descales on E4M3 Q, K and V
+    full = make_inputs(1, 2, 1, 4096, 128, fmt="e4m3", delta=8.0, seed=985)
+    inp = last_queries(full, 32)
+    dev = to_device(inp)
+    ds = (0.75, 1.5, 2.0)
+    for order in ("forward", "reverse"):
+        label = f"kv split fp8qk descales {order}"
+        log(label)
+        gpu = run_gpu(dev, "fp8qk", 256.0, order, True, 128, descales=ds)
+        compare(inp, gpu, "fp8qk", 256.0, order, True, 128, label=label, descales=ds)
+
+
 def test_nocast_and_descales():
     full = make_inputs(1, 2, 1, 300, 128, fmt="f32", delta=7.0, seed=950)
     inp = last_queries(full, 40)
