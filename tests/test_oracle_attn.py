@@ -252,3 +252,68 @@ def test_row_sampling_and_argument_checks():
         oracle.attn(inp.q32, inp.k32, inp.v32, S=0.0, order="forward", block_kv=64)
     with pytest.raises(ValueError):
         oracle.attn(inp.q32, inp.k32, inp.v32, S=1.0, order="forward", block_kv=64, rows=[128])
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("order", ["forward", "reverse"])
+@pytest.mark.parametrize("S", [1.0, 256.0])
+def test_two_level_scores_closed_form(causal, order, S):
+    """Several blocks with the cast on, against a closed form.  q = e_0 and
+    k_t = (X if t < 4 else Y) e_0 give raw scores X on the four sink keys and
+    Y on every other key.  Forward, block 0 fixes the maximum X at once: every
+    non-sink key has P_y = exp2(x_y) and code E(P_y S) (zero at S = 1: the
+    collapse).  Reverse, the later blocks come first with maximum Y (P = 1,
+    code E(S)); block 0 then raises the maximum and rescales O and l by
+    alpha = exp2(fl(Y c) - fl(X c)).  Codes from torch's float8_e4m3fn, sums
+    in FP64.  The oracle accumulates l and O in FP32 over up to 256 equal
+    addends, so the bar is 3e-5 relative (about n u); Y puts P_y S about 4 %
+    away from its E4M3 code, so a plausible slip (l summed over the cast P, a
+    missing alpha, a wrong code) moves the result by 1e-3 or more."""
+    N, d, Bc, X, Y = 256, 64, 64, 64.0, 0.34375
+    rng = np.random.default_rng(31)
+    q = np.zeros((1, 1, N, d), np.float32)
+    q[..., 0] = 1.0
+    k = np.zeros((1, 1, N, d), np.float32)
+    k[0, 0, :, 0] = Y
+    k[0, 0, :4, 0] = X
+    v = rng.standard_normal((1, 1, N, d)).astype(np.float32)
+    out, lse, _ = oracle.attn(q, k, v, S=S, order=order, causal=causal, block_kv=Bc)
+
+    c = c_const(d)
+    f32 = np.float32
+    mcX, mcY = f32(X * c), f32(Y * c)
+
+    def p_of(D, mc):       # P = exp2(fl32(fma(D, c, -mc))), FP64 exp2 rounded once
+        x = f32(np.float64(D) * np.float64(c) - np.float64(mc))
+        return f32(np.exp2(np.float64(x)))
+
+    def code(p):           # decoded E4M3 code of fl32(P S)
+        y = torch.tensor([float(f32(p * f32(S)))], dtype=torch.float32)
+        return float(y.to(torch.float8_e4m3fn).float()[0])
+
+    Ps, Py = p_of(X, mcX), p_of(Y, mcX)           # relative to the sink maximum
+    P1 = p_of(Y, mcY)                              # relative to Y (= 1)
+    alpha = f32(np.exp2(np.float64(mcY) - np.float64(mcX)))
+    vv = v[0, 0].astype(np.float64)
+    for r in range(N):
+        L = r + 1 if causal else N
+        sink = vv[:min(4, L)].sum(0)
+        ns = min(4, L)
+        y0 = vv[ns:min(L, Bc)].sum(0)
+        n0 = min(L, Bc) - ns
+        y1 = vv[Bc:L].sum(0) if L > Bc else np.zeros(d)
+        n1 = max(0, L - Bc)
+        if order == "forward" or n1 == 0:
+            o = code(Ps) * sink + code(Py) * (y0 + y1)
+            ell = ns * np.float64(Ps) + (n0 + n1) * np.float64(Py)
+        else:
+            o = np.float64(alpha) * code(P1) * y1 + code(Ps) * sink + code(Py) * y0
+            ell = np.float64(alpha) * n1 * np.float64(P1) + ns * np.float64(Ps) + n0 * np.float64(Py)
+        want = o / (S * ell)
+        assert np.all(np.abs(out[r] - want) <= 2e-6 + 3e-5 * np.abs(want)), (r, order, causal, S)
+        want_lse = (np.float64(mcX) + math.log2(ell)) * math.log(2.0)
+        assert abs(lse[r] - want_lse) <= 3e-5, (r, order, causal, S)
+    if S == 1.0:
+        assert code(Py) == 0.0          # the non-sink keys collapse under the sink maximum
+    else:
+        assert abs(code(Py) / (np.float64(Py) * S) - 1.0) > 0.03
