@@ -71,6 +71,20 @@ def test_split_over_workgroups(mode, d, bkv, nk):
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
+@pytest.mark.parametrize("mode", ["fast", "fp8qk"])
+def test_split_over_workgroups_gqa(mode):
+    # GQA 8:1 with two batches: 2 * 8 * 2 = 32 tiles of 32 rows against 2500
+    # keys (20 blocks of 128): C = min(256 / 32, 20 / 8, 8) = 2 workgroups per tile
+    full = make_inputs(2, 8, 1, 2500, 128, fmt=FMT[mode], delta=9.0, seed=990)
+    inp = last_queries(full, 50)
+    dev = to_device(inp)
+    for causal, order in itertools.product([False, True], ["forward", "reverse"]):
+        label = f"kv split gqa {mode} causal={causal} {order}"
+        log(label)
+        gpu = run_gpu(dev, mode, 256.0, order, causal, 128)
+        compare(inp, gpu, mode, 256.0, order, causal, 128, label=label)
+
+
 def test_split_over_workgroups_descaled():
     # a split tile (C = 4) with per-tensor descales on E4M3 Q, K and V
     full = make_inputs(1, 2, 1, 4096, 128, fmt="e4m3", delta=8.0, seed=985)
