@@ -299,17 +299,20 @@ def main() -> int:
             out_dyn, _ = A.fwd(q, k, v, S=S, order=order, causal=w.causal, block_kv=w.block_kv,
                                mode=w.mode, want_lse=False, scale="dynamic")
             torch.cuda.synchronize()
-        res["cpu_baseline"] = cpu_baseline(inp, w, order, S, out, cnt_np, sample_rows, out_dyn)
+        res["cpu_baseline"] = cpu_baseline(inp, w, order, S, out, lse, cnt_np, sample_rows, out_dyn)
     print(json.dumps(res), flush=True)
     return 0
 
 
-def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows, out_dyn_dev=None):
+def cpu_baseline(inp, w, order, S, out_dev, lse_dev, cnt_gpu, sample_rows, out_dyn_dev=None):
     """The oracle (as it stands) on a bounded row sample of the same workload,
-    plus P-cast MSE of the GPU output and of the oracle against FP64 attention."""
+    plus P-cast MSE of the GPU output and of the oracle against FP64 attention,
+    the largest GPU-oracle differences, and the sample's underflow fractions
+    per key category next to the paper's collapse fraction F(Delta, S)."""
     import numpy as np
 
     import oracle
+    from oracle import analysis
 
     nthreads = min(16, oracle.default_threads())
     # about 10-15 s of oracle work on 16 host threads at the headline size
@@ -328,6 +331,15 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows, out_dyn_dev=No
     g = out_dev.cpu().numpy().reshape(-1, w.d)[rows]
     mse_gpu = float(np.mean((g.astype(np.float64) - ref) ** 2))
     mse_oracle = float(np.mean((o_out.astype(np.float64) - ref) ** 2))
+    gl = lse_dev.cpu().numpy().reshape(-1)[rows]
+    # visible keys of each sampled row per category: sink keys, the rest of
+    # block 0, the other blocks
+    n_s = np.minimum(inp.n_sink, keys)
+    n_b0 = np.minimum(w.block_kv, keys) - n_s
+    n_o = keys - np.minimum(w.block_kv, keys)
+    frac = {name: (float(o_cnt[:, i].sum() / n.sum()) if n.sum() else None)
+            for i, (name, n) in enumerate((("sink", n_s), ("sink_block_nonsink", n_b0),
+                                           ("other_blocks", n_o)))}
     extra = {}
     if out_dyn_dev is not None:
         gd = out_dyn_dev.cpu().numpy().reshape(-1, w.d)[rows]
@@ -343,6 +355,13 @@ def cpu_baseline(inp, w, order, S, out_dev, cnt_gpu, sample_rows, out_dyn_dev=No
         "mse_gpu_vs_fp64": mse_gpu,
         "mse_oracle_vs_fp64": mse_oracle,
         "max_abs_gpu_minus_oracle": float(np.abs(g - o_out).max()),
+        "max_abs_lse_gpu_minus_oracle": float(np.abs(gl.astype(np.float64) - o_lse).max()),
+        # fraction of the sample's visible (row, key) pairs per category whose
+        # E4M3 code is zero; F(Delta, S) is the paper's collapse fraction of
+        # non-sink keys under the sink maximum (forward order: every block;
+        # reverse order: block 0 only, none elsewhere by Theorem 2)
+        "underflow_fraction": frac,
+        "collapse_fraction_F": analysis.collapse_fraction(inp.delta_eff, S, inp.n_sink),
         "counts_equal_on_sample": bool(np.array_equal(cnt_gpu[rows], o_cnt)),
         **extra,
     }
