@@ -240,9 +240,14 @@ def test_workload_causal_gqa_n131072_fast_bias_full_size():
     heads = np.array([0, 13, 31])
     rows = np.concatenate([h * w.N + np.concatenate([np.arange(0, 64), rng.integers(0, w.N, 48),
                                                      np.arange(w.N - 16, w.N)]) for h in heads])
-    rows = np.unique(rows)
-    label = f"{w.name} S=256 reverse (rows {rows.size})"
-    log(label)
     gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv)
+    # The per-key bias breaks Theorem 2's premise, and some rows have zero
+    # codes outside block 0 even in reverse order at S = 256: up to 16 of
+    # them join the sample (chosen from the device counts; what they must
+    # equal still comes from the oracle)
+    far = np.flatnonzero(gpu[2].reshape(-1, 3)[:, 2] > 0)
+    rows = np.unique(np.concatenate([rows, far[:: max(1, far.size // 16)][:16]]))
+    label = f"{w.name} S=256 reverse (rows {rows.size}, {far.size} with zeros past block 0)"
+    log(label)
     res = compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows, label=label)
     log(str(res))
