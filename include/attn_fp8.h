@@ -57,9 +57,11 @@
  * Ownership and threading: every pointer is a device pointer owned by the
  * caller.  The library keeps no per-call state and is reentrant.  It
  * allocates no memory, except that a KV-cache call whose 32-row tiles cannot
- * fill the GPU takes a temporary workspace (see attn_fp8_fwd_kv): a
- * stream-ordered allocation on `stream`, released the same way before the
- * call returns, so it never outlives the work enqueued by that call.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ * fill the GPU uses a workspace (see attn_fp8_fwd_kv): one per (device,
+ * stream), taken with a stream-ordered allocation on first use, grown the
+ * same way when a call needs more, and kept until the process ends.  Calls on
+ * one stream share it in stream order; calls on different streams never do
+ * (a destroyed stream's handle, if reused, inherits its buffer).  Work is enqueued on `stream` (a hipStream_t; NULL = the null
  * stream) and runs asynchronously: a return of ATTN_OK means "validated and
  * launched"; synchronise on the stream before reading results.
  *
@@ -203,8 +205,8 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
  * the tiles are fewer than the GPU's compute units, each tile is split over
  * C = min(CUs / tiles, blocks / 8, 8) workgroups and the call enqueues three
  * kernels (the range maxima, Algorithm 1 per range, a merge) with a
- * workspace of tiles * C * (8 * 32 + 32 * d + 32) floats taken from a
- * stream-ordered allocation; if that allocation fails the tiles run unsplit
+ * workspace of tiles * C * (8 * 32 + 32 * d + 32) floats, the stream's cached
+ * one (see Ownership above); if it cannot be allocated the tiles run unsplit
  * (same results).  Nq > Nk returns ATTN_ERR_INVALID_ARG; other arguments and
  * return codes as for the descaled entry points.
  */

@@ -1,8 +1,8 @@
 // C ABI of libattn_fp8.so (declared in include/attn_fp8.h): argument
 // validation, choice of kernel instantiation, grid sizing, launch on the
-// caller's stream.  No state is kept; the only memory taken is the prefill
-// kernel's split workspace, allocated and released in stream order on the
-// caller's stream within the call.
+// caller's stream.  No per-call state is kept; the only memory taken is the
+// prefill kernel's split workspace, one per (device, stream), allocated in
+// stream order on first use and kept until the process ends.
 #include "../../include/attn_fp8.h"
 #include "attn_common.hpp"
 #include "attn_launch.hpp"

@@ -41,7 +41,9 @@
 #include "attn_launch.hpp"
 
 #include <math.h>
+#include <mutex>
 #include <type_traits>
+#include <vector>
 
 namespace attn {
 
@@ -664,14 +666,61 @@ hipError_t launch_phase(const Params& p, int d, int block_kv, bool causal, bool 
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Split workspaces: one per (device, stream), grown on demand and kept until
+// the process ends.  Calls on one stream run in stream order, so they can
+// share its buffer; calls on different streams never do.  A buffer that must
+// grow is released in stream order (after the work already enqueued on its
+// stream) and a larger one taken the same way.  Taking and releasing a
+// buffer on every call would cost the host ~35 us per call (the stream-ordered
+// release), more than the split kernels themselves on the Exp. 1 shape.
+struct Workspace {
+    int dev;
+    hipStream_t stream;
+    void* ptr;
+    size_t bytes;
+};
+std::mutex ws_mutex;
+std::vector<Workspace> ws_cache;
+
+void* split_workspace(hipStream_t stream, size_t bytes)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(ws_mutex);
+    Workspace* slot = nullptr;
+    for (Workspace& w : ws_cache)
+        if (w.dev == dev && w.stream == stream)
+            slot = &w;
+    if (slot && slot->bytes >= bytes)
+        return slot->ptr;
+    if (slot) {
+        if (hipFreeAsync(slot->ptr, stream) != hipSuccess)
+            (void)hipGetLastError();
+        slot->ptr = nullptr;
+        slot->bytes = 0;
+    }
+    void* ptr = nullptr;
+    if (hipMallocAsync(&ptr, bytes, stream) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    if (slot) {
+        slot->ptr = ptr;
+        slot->bytes = bytes;
+    } else {
+        ws_cache.push_back({dev, stream, ptr, bytes});
+    }
+    return ptr;
+}
+
 }  // namespace
 
 // Tiles (32 query rows of one batch and head) that cannot fill the chip are
 // split over C workgroups each: C = min(n_cu / tiles, blocks / 8, 8), so that
 // every wave range holds at least one KV block.  The split needs a workspace
-// (range maxima, per-workgroup partial sums), taken with a stream-ordered
-// allocation on the caller's stream and released the same way after the
-// three launches; if that allocation fails the tile runs unsplit.
+// (range maxima, per-workgroup partial sums): the stream's cached one
+// (split_workspace); if it cannot be had the tile runs unsplit.
 hipError_t launch_prefill(const Params& p_in, int d, int block_kv, bool causal, bool count, int scale,
                           bool qk8, int n_cu, hipStream_t stream)
 {
@@ -700,11 +749,9 @@ hipError_t launch_prefill(const Params& p_in, int d, int block_kv, bool causal, 
         const size_t n_part = (size_t)units * C * (32 * (size_t)d + 32);
         off_part = align256(n_max * sizeof(float));
         const size_t bytes = off_part + align256(n_part * sizeof(float));
-        if (hipMallocAsync(&ws, bytes, stream) != hipSuccess) {
-            (void)hipGetLastError();
-            ws = nullptr;
+        ws = split_workspace(stream, bytes);
+        if (!ws)
             C = 1;
-        }
     }
     if (C == 1) {
         p.total_wg = (int)units;
@@ -731,8 +778,7 @@ hipError_t launch_prefill(const Params& p_in, int d, int block_kv, bool causal, 
             hipLaunchKernelGGL(prefill_merge<128>, dim3((unsigned)(units * 8)), dim3(128), 0, stream, p);
         e = hipGetLastError();
     }
-    const hipError_t ef = hipFreeAsync(ws, stream);
-    return e != hipSuccess ? e : ef;
+    return e;
 }
 
 int prefill_rows_per_wg() { return 32; }

@@ -149,3 +149,34 @@ def test_square_call_through_kv_entry_is_unchanged():
     torch.cuda.synchronize()
     assert st == 0
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_split_workspace_growth_and_streams():
+    # The split prefill keeps one workspace per (device, stream).  A small
+    # split, a larger one (the workspace grows) and the small one again on
+    # one stream; then the two problems enqueued back to back on two streams
+    # (separate workspaces).  Every result equals the oracle.
+    import torch
+    from paper_2606_06521_amd import attn_fp8 as A
+    small = last_queries(make_inputs(1, 2, 1, 2000, 128, fmt="bf16_e4m3", delta=8.0, seed=995), 20)
+    large = last_queries(make_inputs(4, 4, 2, 4096, 128, fmt="bf16_e4m3", delta=8.0, seed=996), 40)
+    dsmall, dlarge = to_device(small), to_device(large)
+
+    def run(dev, stream):
+        with torch.cuda.stream(stream):
+            q, k, v = dev
+            o, l = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
+        return o, l
+
+    s0 = torch.cuda.current_stream()
+    outs = [(small, run(dsmall, s0)), (large, run(dlarge, s0)), (small, run(dsmall, s0))]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(s0)
+    s2.wait_stream(s0)
+    outs += [(small, run(dsmall, s1)), (large, run(dlarge, s2))]
+    torch.cuda.synchronize()
+    for i, (inp, (o, l)) in enumerate(outs):
+        label = f"kv split workspace call {i}"
+        log(label)
+        gpu = (o.cpu().numpy(), l.cpu().numpy(), None)
+        compare(inp, gpu, "fast", 256.0, "reverse", True, 128, label=label)
