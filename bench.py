@@ -145,8 +145,8 @@ def main() -> int:
         return 0
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build runs on one GPU only; the path shards over (batch, KV-head) "
-              "groups with no communication, so multi-GPU throughput is not measured here.",
+        print("bench.py: measures one GPU only; the attention path shards over (batch, KV-head) "
+              "groups with no communication, so a multi-GPU figure is not measured.",
               file=sys.stderr)
         return 2
 

@@ -48,3 +48,15 @@ def test_measured_traffic_only_for_the_current_sources(tmp_path, monkeypatch):
     assert bench.measured_traffic("other") is None                  # another workload
     path.write_text(json.dumps(dict(rec, kernel_source_sha256="0" * 64)))
     assert bench.measured_traffic("wl") is None                     # kernels changed since
+
+
+def test_more_than_one_gpu_is_refused_with_a_message():
+    # one GPU only: --gpus N > 1 exits non-zero before touching a device
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode != 0
+    assert "one GPU" in r.stderr and r.stdout == ""
