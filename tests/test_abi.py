@@ -180,3 +180,32 @@ def test_misaligned_pointers_are_rejected(A):
     cnt = A.attn_fp8_p_underflow_count(base, base, base, 1, 2, 1, 64, 64, 0, 64, 0, 256.0, 1, 4,
                                        base + 1, None, None, None)
     assert cnt == -1
+
+
+def test_header_is_plain_c_and_links(A, tmp_path):
+    # a C99 program that includes the header, links the library and calls the
+    # entry points that need no GPU (version, strerror, a validation error)
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_abi.c"
+    src.write_text(r'''
+#include <stdio.h>
+#include "attn_fp8.h"
+int main(void) {
+    int st = attn_fp8_fwd(0, 0, 0, 0, 0, -1, 1, 1, 8, 64, 0, 64, 0, 256.0f, 1, 0);
+    printf("%d %d %s\n", attn_fp8_version(), st == ATTN_ERR_INVALID_ARG, attn_fp8_strerror(st));
+    return st == ATTN_ERR_INVALID_ARG ? 0 : 1;
+}
+''')
+    exe = tmp_path / "use_abi"
+    libdir = os.path.dirname(A.LIB_PATH)
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-pedantic-errors", "-I", os.path.join(ROOT, "include"),
+                    str(src), "-o", str(exe), "-L", libdir, "-lattn_fp8", "-Wl,-rpath," + libdir],
+                   check=True, capture_output=True, text=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    version, rejected, _ = r.stdout.split(" ", 2)
+    assert int(version) == A.attn_fp8_version() and rejected == "1"
