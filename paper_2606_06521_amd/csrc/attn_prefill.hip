@@ -17,8 +17,8 @@
 //   merge:  the eight (O, l) partials are brought to the row's final maximum
 //           (one exp2 each) and summed.  Only the FP32 rounding of O and l
 //           differs from the sequential chain of alpha products.
-// The scores are computed twice (once per pass); the second read of K comes
-// from L2.
+// The scores are computed twice (once per pass); K is read twice (the
+// counters show both reads reaching HBM at the Exp. 1 shape).
 //
 // When the tiles alone cannot fill the chip, each tile is split over nsplit
 // workgroups (the visit order cut into nsplit * 8 contiguous wave ranges) and
@@ -34,9 +34,10 @@
 // PHASE 0 is the one-workgroup kernel with both passes fused.
 //
 // K fragments (the S^T MFMA's A operand) are read straight from HBM, 16
-// bytes per lane, in the key order of a_row_to_key.  Each wave stages the V
-// block it multiplies in its own LDS region, in the XOR-swizzled layout read
-// transposed by ds_read_b64_tr_b8 (as in the fast kernel).
+// bytes per lane, in the key order of a_row_to_key.  Each wave copies the V
+// block it multiplies straight into its own LDS region (global_load_lds, no
+// register staging), in the XOR-swizzled layout read transposed by
+// ds_read_b64_tr_b8 (as in the fast kernel).
 #include "attn_common.hpp"
 #include "attn_launch.hpp"
 
