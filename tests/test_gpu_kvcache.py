@@ -180,3 +180,42 @@ def test_split_workspace_growth_and_streams():
         log(label)
         gpu = (o.cpu().numpy(), l.cpu().numpy(), None)
         compare(inp, gpu, "fast", 256.0, "reverse", True, 128, label=label)
+
+
+def test_split_workspace_two_host_threads():
+    # Two host threads, each on its own stream, enqueue different split
+    # problems over and over (ctypes releases the GIL during the calls, so
+    # the workspace cache is entered concurrently); every thread's last
+    # result equals the oracle.
+    import threading
+    import torch
+    from paper_2606_06521_amd import attn_fp8 as A
+    probs = [last_queries(make_inputs(1, 2, 1, 2500, 128, fmt="bf16_e4m3", delta=8.0, seed=997), 24),
+             last_queries(make_inputs(2, 4, 2, 3000, 128, fmt="bf16_e4m3", delta=9.0, seed=998), 33)]
+    devs = [to_device(p) for p in probs]
+    results = [None, None]
+    errors = []
+
+    def worker(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                q, k, v = devs[i]
+                for _ in range(20):
+                    o, l = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
+                s.synchronize()
+                results[i] = (o.cpu().numpy(), l.cpu().numpy(), None)
+        except Exception as e:   # surfaced below
+            errors.append(e)
+
+    torch.cuda.synchronize()
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i in range(2):
+        label = f"kv split two threads, problem {i}"
+        log(label)
+        compare(probs[i], results[i], "fast", 256.0, "reverse", True, 128, label=label)
