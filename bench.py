@@ -8,8 +8,8 @@ tensors already resident in HBM when the timed region starts.
 Prints ONE JSON line:
   value      whole-job TFLOP/s (FlashAttention convention 4*B*H*N^2*d, halved
              under causal masking) over K timed steps bracketed by device syncs;
-  roofline   the attention kernel's algorithmic FLOPs per launch divided by its
-             average launch time from HIP events on its stream, against the
+  roofline   the attention kernel's algorithmic FLOPs per launch divided by the
+             median of its launch times from HIP events on its stream, against the
              dense FP8 MFMA peak (and, for reference, the mixed bf16+FP8 peak
              this kernel's instruction mix can reach);
   cpu_baseline  the CPU oracle timed on a bounded row sample of the same
@@ -196,11 +196,15 @@ def main() -> int:
     mode = A.MODES[w.mode]
     ordc = A.ORDERS[order]
     ptrs = (q.data_ptr(), k.data_ptr(), v.data_ptr(), out.data_ptr(), lse.data_ptr())
+    # the KV-cache split's workspace (the caller's memory), taken once
+    ws = A.kv_workspace(w.B, w.Hq, w.Hkv, w.rows, w.N, w.d, w.causal, w.block_kv, mode,
+                        q.device) if w.nq else None
+    ws_ptr, ws_bytes = (None, 0) if ws is None else (ws.data_ptr(), ws.numel())
 
     def step():
         if w.nq:
             st = A.attn_fp8_fwd_kv(*ptrs, w.B, w.Hq, w.Hkv, w.rows, w.N, w.d, int(w.causal),
-                                   w.block_kv, ordc, S, mode, 1.0, 1.0, 1.0, sptr)
+                                   w.block_kv, ordc, S, mode, 1.0, 1.0, 1.0, ws_ptr, ws_bytes, sptr)
         else:
             st = A.attn_fp8_fwd(*ptrs, w.B, w.Hq, w.Hkv, w.N, w.d, int(w.causal), w.block_kv,
                                 ordc, S, mode, sptr)
@@ -221,19 +225,25 @@ def main() -> int:
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     kernel_ms = [s_ev.elapsed_time(e_ev) for s_ev, e_ev in ev]
-    kernel_ms_avg = float(np.mean(kernel_ms))
+    # the statistic of the roofline: the median of the timed launches (mean
+    # and minimum reported beside it)
+    kernel_ms_med = float(np.median(kernel_ms))
     flops = w.flops()
     # dense peak of the contraction dtype: FP8 MFMA for the fast modes (the
     # spec denominator), FP32 matrix for the faithful ones
     peak = PEAK_TFLOPS["fp8"] if w.mode in ("fast", "fp8qk") else 157.3
     value = flops / (ms_per_step * 1e-3) / 1e12
-    achieved = flops / (kernel_ms_avg * 1e-3) / 1e12
+    achieved = flops / (kernel_ms_med * 1e-3) / 1e12
     # algorithmic HBM bytes: q, k, v once, out and lse written once
     qk_bytes = 1 if w.fmt == "e4m3" else (2 if w.fmt == "bf16_e4m3" else 4)
     v_bytes = 4 if w.fmt == "f32" else 1
     hbm_bytes = float(w.B * (w.Hq * w.rows * w.d * qk_bytes + w.Hkv * w.N * w.d * (qk_bytes + v_bytes)
                              + w.Hq * w.rows * (4 * w.d + 4)))
     hbm_bound = flops / hbm_bytes < peak / HBM_PEAK_GBS * 1e3
+    timing = {"kernel_ms_median": round(kernel_ms_med, 4),
+              "kernel_ms_mean": round(float(np.mean(kernel_ms)), 4),
+              "kernel_ms_min": round(float(np.min(kernel_ms)), 4),
+              "timed_launches": len(kernel_ms)}
 
     # P-underflow diagnostic on the same inputs (timed separately, not reported as throughput)
     cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=w.causal, block_kv=w.block_kv,
@@ -261,13 +271,13 @@ def main() -> int:
                    "S": S, "delta_eff": round(inp.delta_eff, 4), "parallelism": "single GPU"},
         "roofline": {
             "bound": "hbm",
-            "achieved": round(hbm_bytes / (kernel_ms_avg * 1e-3) / 1e9, 1),
+            "achieved": round(hbm_bytes / (kernel_ms_med * 1e-3) / 1e9, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(hbm_bytes / (kernel_ms_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "frac": round(hbm_bytes / (kernel_ms_med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "algorithmic_bytes_per_launch": hbm_bytes,
             "traffic": measured_traffic(w.name),
-            "kernel_ms_avg": round(kernel_ms_avg, 4),
+            **timing,
             "flops_per_launch": flops,
             "tflops": round(achieved, 2),
         } if hbm_bound else {
@@ -277,16 +287,16 @@ def main() -> int:
             "unit": "TFLOP/s",
             "frac": round(achieved / peak, 4),
             "traffic": measured_traffic(w.name),
-            "kernel_ms_avg": round(kernel_ms_avg, 4),
+            **timing,
             "flops_per_launch": flops,
             "mixed_bf16_fp8_peak": round(MIXED_PEAK, 1) if w.mode == "fast" else None,
             "frac_of_mixed_peak": round(achieved / MIXED_PEAK, 4) if w.mode == "fast" else None,
         },
         # one exp2 per visible (row, key) pair, against the measured v_exp_f32 rate
         "exp2": {"per_launch": w.pairs(),
-                 "achieved_per_s": float("%.4g" % (w.pairs() / (kernel_ms_avg * 1e-3))),
+                 "achieved_per_s": float("%.4g" % (w.pairs() / (kernel_ms_med * 1e-3))),
                  "peak_per_s": EXP2_PEAK_PER_S,
-                 "frac": round(w.pairs() / (kernel_ms_avg * 1e-3) / EXP2_PEAK_PER_S, 4)},
+                 "frac": round(w.pairs() / (kernel_ms_med * 1e-3) / EXP2_PEAK_PER_S, 4)},
         "p_underflow_counts": {"sink": counts_total[0], "sink_block_nonsink": counts_total[1],
                                "other_blocks": counts_total[2]},
         "input_gen_s": round(gen_s, 2),

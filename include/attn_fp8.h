@@ -3,26 +3,27 @@
  * for AMD Instinct MI355X (gfx950), with a static P-scale S and a runtime
  * KV-block iteration order.
  *
- * The operation is Algorithm 1 of "P-Cast Precision in FP8 Attention:
- * Sink-Induced Collapse and the Optimality of S = 2^8" (Sec. 2.2), applied to
- * every query row of every (batch, head), with the kernel semantics of
- * Sec. 6.1:
- *   for each KV block j in the chosen order:
- *     Z     = Q K_j^T / sqrt(d)                        (FP32 scores)
- *     m_new = max(m, max Z);  alpha = exp(m - m_new)
- *     P     = exp(Z - m_new)                           (FP32)
- *     l     = alpha * l + sum(P)                       (pre-cast P)
- *     P8    = cast_E4M3(P * S)                         (round to nearest even)
- *     O     = alpha * O + P8 . V_j                     (FP32 accumulator)
- *   out = O / (S * l)
- * Base-2 form used on the device: with c = fl32(log2(e)/sqrt(d)) and D the
- * raw dot product q.k, mc = fl(m*c), x = fma(D, c, -mc), P = exp2(x),
- * alpha = exp2(mc_old - mc_new).  KV blocks are [j*block_kv, (j+1)*block_kv)
- * anchored at key 0; ORDER_FORWARD visits j = 0, 1, ...; ORDER_REVERSE visits
- * the last block first and the sink block (block 0) last (Sec. 4.1).  Under
- * causal masking, row r sees keys t <= r only and visits only the blocks that
- * hold at least one such key; masked keys take no part in l, O or the counts.
- * The running maximum is updated once per KV block, never lazily.
+ * The operation is the FP8 online-softmax attention of Algorithm 1 in
+ * "P-Cast Precision in FP8 Attention: Sink-Induced Collapse and the Optimality
+ * of S = 2^8" (Sec. 2.2), applied to every query row of every (batch, head),
+ * with the kernel semantics of Sec. 6.1.  Each row keeps a running maximum of
+ * its scores, a running sum l and an FP32 output accumulator, and visits its
+ * KV blocks one at a time in the chosen order.  Per block, the maximum is
+ * raised to cover the block's scores and the old l and accumulator are
+ * rescaled to it; l then adds the block's softmax numerators P in FP32
+ * before any cast (the normaliser is exact), while the accumulator adds
+ * products of V with the E4M3 codes of P * S (round to nearest even), so the
+ * cast error sits in the numerator alone.  The result is the accumulator
+ * divided by S * l.
+ * The device works in base 2: with c = fl32(log2(e)/sqrt(d)) and D the raw
+ * dot product q.k, mc = fl(m*c), x = fma(D, c, -mc), P = exp2(x), and the
+ * rescale factor is exp2(mc_old - mc_new).  KV blocks are [j*block_kv,
+ * (j+1)*block_kv) anchored at key 0; ATTN_ORDER_FORWARD visits j = 0, 1, ...;
+ * ATTN_ORDER_REVERSE visits the last block first and the sink block (block 0)
+ * last (Sec. 4.1).  Under causal masking, row r sees keys t <= r only and
+ * visits only the blocks that hold at least one such key; masked keys take
+ * no part in l, the accumulator or the counts.  The running maximum is
+ * updated once per KV block, never lazily.
  *
  * Memory layout (all contiguous, row-major, device memory owned by the caller):
  *   q    [B][Hq][N][d]
@@ -55,15 +56,12 @@
  * otherwise ATTN_ERR_INVALID_ARG.
  *
  * Ownership and threading: every pointer is a device pointer owned by the
- * caller.  The library keeps no per-call state and is reentrant.  It
- * allocates no memory, except that a KV-cache call whose 32-row tiles cannot
- * fill the GPU uses a workspace (see attn_fp8_fwd_kv): one per (device,
- * stream), taken with a stream-ordered allocation on first use, grown the
- * same way when a call needs more, and kept until the process ends.  Calls on
- * one stream share it in stream order; calls on different streams never do
- * (a destroyed stream's handle, if reused, inherits its buffer).  Work is enqueued on `stream` (a hipStream_t; NULL = the null
- * stream) and runs asynchronously: a return of ATTN_OK means "validated and
- * launched"; synchronise on the stream before reading results.
+ * caller.  The library allocates no memory and keeps no state between calls;
+ * it is reentrant.  The one scratch buffer a call can use, the workspace of a
+ * KV-cache call whose 32-row tiles cannot fill the GPU (see attn_fp8_fwd_kv),
+ * is passed in by the caller.  Work is enqueued on `stream` (a hipStream_t;
+ * NULL = the null stream) and runs asynchronously: a return of ATTN_OK means
+ * "validated and launched"; synchronise on the stream before reading results.
  *
  * Errors: arguments are validated before any HIP call; on failure nothing is
  * launched and the return value says why.  A launch failure reported by the
@@ -72,6 +70,7 @@
 #ifndef ATTN_FP8_H
 #define ATTN_FP8_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -144,7 +143,8 @@ int attn_fp8_fwd(const void* q, const void* k, const void* v, float* out,
  *                                                     the sink's KV block)
  *   counts[row][2]: keys t >= block_kv               (all other blocks)
  *   counts    device uint32 [B][Hq][N][3]; required; every entry is written.
- *   n_sink    >= 0.
+ *   n_sink    0 <= n_sink <= block_kv (the sink keys lie in block 0, so the
+ *             three categories are disjoint); else ATTN_ERR_INVALID_ARG.
  *   out, lse  optional (NULL allowed); when given they receive the same
  *             values attn_fp8_fwd writes.
  * Other arguments and return codes as for attn_fp8_fwd.
@@ -202,24 +202,48 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
  * before it, so the P codes are those of the sequential visit; only the FP32
  * summation order of O and l differs.  (Long chunks, Nq >= 128 with Nk - Nq a
  * multiple of block_kv, run on the square problem's kernel instead.)  When
- * the tiles are fewer than the GPU's compute units, each tile is split over
- * C = min(CUs / tiles, blocks / 8, 8) workgroups and the call enqueues three
- * kernels (the range maxima, Algorithm 1 per range, a merge) with a
- * workspace of tiles * C * (8 * 32 + 32 * d + 32) floats, the stream's cached
- * one (see Ownership above); if it cannot be allocated the tiles run unsplit
- * (same results).  Nq > Nk returns ATTN_ERR_INVALID_ARG; other arguments and
- * return codes as for the descaled entry points.
+ * the tiles are fewer than the GPU's compute units, each tile can be split
+ * over C = min(CUs / tiles, blocks / 8, 8) workgroups; the call then enqueues
+ * three kernels (the range maxima, Algorithm 1 per range, a merge) and needs
+ * a device workspace of attn_fp8_kv_workspace_bytes() bytes:
+ *   workspace        device memory of the caller, 256-byte aligned, or NULL.
+ *                    The call uses it as scratch on `stream` (no contents are
+ *                    read before the call writes them); calls that overlap in
+ *                    time must not share one.  NULL runs the tiles unsplit
+ *                    (same results, fewer workgroups).
+ *   workspace_bytes  its size; with a non-NULL workspace it must be at least
+ *                    what attn_fp8_kv_workspace_bytes reports for the same
+ *                    shape on the current device, else ATTN_ERR_INVALID_ARG.
+ * Nq > Nk returns ATTN_ERR_INVALID_ARG; other arguments and return codes as
+ * for the descaled entry points.
  */
 int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse,
                     int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
                     int block_kv, int order, float S, int mode, float q_descale,
-                    float k_descale, float v_descale, void* stream);
+                    float k_descale, float v_descale, void* workspace,
+                    size_t workspace_bytes, void* stream);
 
 int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, int B,
                                   int Hq, int Hkv, int Nq, int Nk, int d, int causal,
                                   int block_kv, int order, float S, int mode, int n_sink,
                                   float q_descale, float k_descale, float v_descale,
-                                  uint32_t* counts, float* out, float* lse, void* stream);
+                                  uint32_t* counts, float* out, float* lse,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace the KV-cache entry points can use for the shape (B, Hq, Hkv, Nq,
+ * Nk, d, causal, block_kv, mode) on the current device: *bytes is set to 0
+ * when the call would not split (square problems, long chunks, faithful
+ * modes, tiles enough to fill the GPU), else to the size of the range maxima
+ * (tiles * C * 8 * 32 floats) plus, from a 256-byte boundary, the partial
+ * sums (tiles * C * (32 d + 32) floats).  Since tiles * C never exceeds the
+ * CU count, this stays below CUs * (32 d + 288) * 4 + 512 bytes (4.5 MB on a
+ * 256-CU MI355X at d = 128).  Queries the device's CU count; launches nothing.
+ * Returns ATTN_OK, ATTN_ERR_INVALID_ARG (bad shape, NULL bytes),
+ * ATTN_ERR_UNSUPPORTED, or ATTN_ERR_HIP if the device cannot be queried.
+ */
+int attn_fp8_kv_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                                int block_kv, int mode, size_t* bytes);
 
 /*
  * Per-block diagnostic: where each KV block sits below the running maximum,

@@ -19,62 +19,73 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "oracle.c")
 _LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# test build with the planted exp2 error compiled in (-DORACLE_TEST_PLANTS);
+# used only by the code-ambiguity bound's own tests
+_PLANT_PATH = os.path.join(_HERE, "liboracle_plant.so")
 _lib = None
+_plant_lib = None
 
 ORDER = {"forward": 0, "reverse": 1}
 SCALE = {"static": 0, "dynamic": 1}
 
 
+CFLAGS = ["-O2", "-std=c11", "-fno-fast-math", "-ffp-contract=off", "-fPIC", "-shared",
+          "-pthread"]
+
+
+def _compile(path: str, extra=()) -> None:
+    tmp = path + ".tmp%d" % os.getpid()
+    cmd = ["gcc", *CFLAGS, *extra, "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, path)
+
+
 def build(force: bool = True) -> str:
-    """Compile liboracle.so with gcc (no fast-math, no FMA contraction)."""
+    """Compile liboracle.so with gcc (no fast-math, no FMA contraction), and
+    the test build liboracle_plant.so."""
     if force or not os.path.exists(_LIB_PATH):
-        tmp = _LIB_PATH + ".tmp%d" % os.getpid()
-        cmd = ["gcc", "-O2", "-std=c11", "-fno-fast-math", "-ffp-contract=off",
-               "-fPIC", "-shared", "-pthread", "-o", tmp, _SRC, "-lm"]
-        subprocess.run(cmd, check=True)
-        os.replace(tmp, _LIB_PATH)
+        _compile(_LIB_PATH)
+    if force or not os.path.exists(_PLANT_PATH):
+        _compile(_PLANT_PATH, ["-DORACLE_TEST_PLANTS"])
     return _LIB_PATH
+
+
+def _declare(L: ctypes.CDLL) -> ctypes.CDLL:
+    P = ctypes.c_void_p
+    i32, i64, f32, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+    L.oracle_e4m3_encode.argtypes = [f32]
+    L.oracle_e4m3_encode.restype = ctypes.c_uint8
+    L.oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
+    L.oracle_e4m3_decode.restype = f32
+    L.oracle_e4m3_encode_array.argtypes = [P, P, i64]
+    L.oracle_e4m3_encode_array.restype = None
+    L.oracle_e4m3_decode_array.argtypes = [P, P, i64]
+    L.oracle_e4m3_decode_array.restype = None
+    L.oracle_attn_full.argtypes = ([P] * 9 + [i32] + [i32] * 9 + [f32, i32, i32, i32]
+                                   + [f32, f32, f32, f64, f64, P, i64, i32])
+    L.oracle_attn_full.restype = i32
+    L.oracle_ref_fp64_kv.argtypes = [P, P, P, P, P] + [i32] * 7 + [f64, f64, f64, P, i64, i32]
+    L.oracle_ref_fp64_kv.restype = i32
+    L.oracle_version.restype = i32
+    return L
+
+
+def plant_lib() -> ctypes.CDLL:
+    """The test build (planted exp2 error available through jitter_rel)."""
+    global _plant_lib
+    if _plant_lib is None:
+        if not os.path.exists(_PLANT_PATH):
+            _compile(_PLANT_PATH, ["-DORACLE_TEST_PLANTS"])
+        _plant_lib = _declare(ctypes.CDLL(_PLANT_PATH))
+    return _plant_lib
 
 
 def lib() -> ctypes.CDLL:
     global _lib
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
-            build(force=False)
-        L = ctypes.CDLL(_LIB_PATH)
-        P = ctypes.c_void_p
-        i32, i64, f32 = ctypes.c_int, ctypes.c_int64, ctypes.c_float
-        L.oracle_e4m3_encode.argtypes = [f32]
-        L.oracle_e4m3_encode.restype = ctypes.c_uint8
-        L.oracle_e4m3_decode.argtypes = [ctypes.c_uint8]
-        L.oracle_e4m3_decode.restype = f32
-        L.oracle_e4m3_encode_array.argtypes = [P, P, i64]
-        L.oracle_e4m3_encode_array.restype = None
-        L.oracle_e4m3_decode_array.argtypes = [P, P, i64]
-        L.oracle_e4m3_decode_array.restype = None
-        L.oracle_attn.argtypes = [P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, i32, P, i64, i32]
-        L.oracle_attn.restype = i32
-        L.oracle_attn_descaled.argtypes = ([P, P, P, P, P, P] + [i32] * 8 + [f32, i32, i32, i32]
-                                           + [f32, f32, f32, P, i64, i32])
-        L.oracle_attn_descaled.restype = i32
-        f64 = ctypes.c_double
-        L.oracle_attn_bound.argtypes = ([P] * 7 + [i32] * 8 + [f32, i32, i32, i32]
-                                        + [f32, f32, f32, f64, f64, P, i64, i32])
-        L.oracle_attn_bound.restype = i32
-        L.oracle_attn_diag.argtypes = ([P] * 9 + [i32] + [i32] * 8 + [f32, i32, i32, i32]
-                                       + [f32, f32, f32, f64, f64, P, i64, i32])
-        L.oracle_attn_diag.restype = i32
-        L.oracle_attn_full.argtypes = ([P] * 9 + [i32] + [i32] * 9 + [f32, i32, i32, i32]
-                                       + [f32, f32, f32, f64, f64, P, i64, i32])
-        L.oracle_attn_full.restype = i32
-        L.oracle_ref_fp64_kv.argtypes = [P, P, P, P, P] + [i32] * 7 + [f64, f64, f64, P, i64, i32]
-        L.oracle_ref_fp64_kv.restype = i32
-        L.oracle_ref_fp64.argtypes = [P, P, P, P, P] + [i32] * 6 + [P, i64, i32]
-        L.oracle_ref_fp64.restype = i32
-        L.oracle_ref_fp64_descaled.argtypes = [P, P, P, P, P] + [i32] * 6 + [f64, f64, f64, P, i64, i32]
-        L.oracle_ref_fp64_descaled.restype = i32
-        L.oracle_version.restype = i32
-        _lib = L
+            _compile(_LIB_PATH)
+        _lib = _declare(ctypes.CDLL(_LIB_PATH))
     return _lib
 
 
@@ -121,8 +132,9 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     descales: per-tensor (q, k, v) descales of the stored values (Sec. 6.1).
     bound_rel: if given, also return amb [n_rows,d], the bound on how far out
     can move when every P*S within bound_rel (relative) of an E4M3 rounding
-    midpoint takes the other code (see oracle_attn_bound in oracle.c).
-    jitter_rel: planted exp2 error for the bound's own tests; 0 otherwise.
+    midpoint takes the other code (see oracle_attn_full in oracle.c).
+    jitter_rel: planted exp2 error for the bound's own tests (runs the test
+    build liboracle_plant.so); 0 for the method itself.
     Returns (out [n_rows,d] float32, lse [n_rows] float32, counts [n_rows,3]
     uint32[, amb [n_rows,d] float32]).
     """
@@ -142,12 +154,13 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
     counts = np.zeros((n_rows, 3), dtype=np.uint32)
     amb = None if bound_rel is None else np.empty((n_rows, d), dtype=np.float32)
     qd, kd, vd = (float(x) for x in descales)
-    rc = lib().oracle_attn_full(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
-                                _ptr(amb), None, None, 0, B, Hq, Hkv, Nq, Nk, d,
-                                int(bool(causal)), int(block_kv), ORDER[order], float(S),
-                                int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd,
-                                float(bound_rel or 0.0), float(jitter_rel), _ptr(rows_a), n_rows,
-                                nthreads or default_threads())
+    L = plant_lib() if jitter_rel else lib()
+    rc = L.oracle_attn_full(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), _ptr(counts),
+                            _ptr(amb), None, None, 0, B, Hq, Hkv, Nq, Nk, d,
+                            int(bool(causal)), int(block_kv), ORDER[order], float(S),
+                            int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd,
+                            float(bound_rel or 0.0), float(jitter_rel), _ptr(rows_a), n_rows,
+                            nthreads or default_threads())
     if rc != 0:
         raise ValueError("oracle_attn rejected its arguments")
     if amb is not None:
@@ -158,7 +171,7 @@ def attn(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
 def block_diag(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = False,
                cast: bool = True, n_sink: int = 4, rows=None, nthreads: int | None = None,
                scale: str = "static", descales=(1.0, 1.0, 1.0), nbins: int = 32):
-    """Algorithm 1 with the per-block diagnostic (see oracle_attn_diag in
+    """Algorithm 1 with the per-block diagnostic (see oracle_attn_full in
     oracle.c), accumulated over the given rows.
     Returns (out, lse, counts, gap_hist [B,Hq,nblk,nbins] uint32,
     blk_zero [B,Hq,nblk] uint32)."""
@@ -186,7 +199,7 @@ def block_diag(q, k, v, *, S: float, order: str, block_kv: int, causal: bool = F
                                 int(bool(cast)), SCALE[scale], int(n_sink), qd, kd, vd, 0.0, 0.0,
                                 _ptr(rows_a), n_rows, nthreads or default_threads())
     if rc != 0:
-        raise ValueError("oracle_attn_diag rejected its arguments")
+        raise ValueError("oracle_attn_full rejected its arguments")
     return out, lse, counts, hist, bz
 
 

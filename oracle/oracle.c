@@ -51,7 +51,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define ORACLE_VERSION 5
+#define ORACLE_VERSION 6
 
 /* ------------------------------------------------------------------------- */
 /* OCP E4M3 (Sec. 2.1)                                                        */
@@ -154,7 +154,7 @@ typedef struct {
     float v_descale;
     float* amb;         /* [n_rows][d] code-ambiguity bound (nullable) */
     double amb_rel;     /* relative half-width of the ambiguity window */
-    double jitter_rel;  /* planted exp2 error, test use only (0 = none) */
+    double jitter_rel;  /* planted exp2 error (test build only; else 0) */
     uint32_t* gap_hist; /* [B*Hq][nblk_all][nbins] (nullable) */
     uint32_t* blk_zero; /* [B*Hq][nblk_all] (nullable with gap_hist) */
     int nbins, nblk_all;
@@ -165,7 +165,10 @@ typedef struct {
     pthread_mutex_t lock;
 } attn_job;
 
-/* splitmix64 finaliser: a fixed hash of (row, key) for the planted jitter */
+#ifdef ORACLE_TEST_PLANTS
+/* Test build only (liboracle_plant.so, -DORACLE_TEST_PLANTS): a planted exp2
+ * error, so that the code-ambiguity bound can be checked against a known
+ * perturbation.  splitmix64 finaliser: a fixed hash of (row, key). */
 static uint64_t mix64(uint64_t z)
 {
     z += 0x9E3779B97F4A7C15ull;
@@ -173,6 +176,13 @@ static uint64_t mix64(uint64_t z)
     z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
     return z ^ (z >> 31);
 }
+
+static double planted_exp2_error(const attn_job* J, int64_t flat, int key)
+{
+    const uint64_t h = mix64(((uint64_t)flat << 32) ^ (uint64_t)key);
+    return 1.0 + J->jitter_rel * (2.0 * ((double)(h >> 11) * 0x1p-53) - 1.0);
+}
+#endif
 
 static void attn_row(const attn_job* J, int64_t flat, float* out_row,
                      float* lse_row, uint32_t* cnt_row, float* amb_row, float* D,
@@ -199,7 +209,8 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
     const int L = J->causal ? Nk - Nq + r + 1 : Nk;    /* valid keys 0..L-1 */
     const int nblk = (L + Bc - 1) / Bc;
 
-    /* line: m <- -inf, l <- 0, O <- 0 (FP32) */
+    /* running state of the row, FP32: maximum of the raw dots (and its
+     * scaled copy mc = fl(m c)), the pre-cast sum l and the accumulator o */
     float m = -INFINITY, mc = -INFINITY, ell = 0.0f;
     for (int i = 0; i < d; i++)
         o[i] = a[i] = 0.0f;
@@ -207,7 +218,7 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         cnt_row[0] = cnt_row[1] = cnt_row[2] = 0;
 
     for (int it = 0; it < nblk; it++) {
-        /* BlockOrder: forward 0..nblk-1, reverse nblk-1..0 */
+        /* blocks in ascending order, or descending for the reverse order */
         const int j = (J->order == ORDER_FORWARD) ? it : nblk - 1 - it;
         const int t0 = j * Bc;
         const int t1 = (t0 + Bc < L) ? t0 + Bc : L;
@@ -224,7 +235,9 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
             if (D[t] > mloc)
                 mloc = D[t];
         }
-        /* m_new = max(m, m_loc); alpha = exp(m - m_new) in base 2 */
+        /* new running maximum; the rescale factor of the old state is the
+         * base-2 exponential of the difference of the scaled maxima (1
+         * exactly when the maximum does not move, 0 on the first block) */
         const float m_new = (m > mloc) ? m : mloc;
         const float mc_new = m_new * c;
         const float alpha = (float)exp2((double)(mc - mc_new));
@@ -238,15 +251,16 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
                                1u, __ATOMIC_RELAXED);
         }
 
-        /* P = exp(Z - m_new) in FP32, l <- alpha*l + sum(P) (pre-cast) */
+        /* P of every key in FP32 (exp2 in double, rounded once); the sum l
+         * takes these pre-cast values (Sec. 6.1) */
         float psum = 0.0f;
         for (int t = 0; t < nt; t++) {
             const float x = fmaf(D[t], c, -mc_new);
             double e = exp2((double)x);
-            if (J->jitter_rel != 0.0) {
-                const uint64_t h = mix64(((uint64_t)flat << 32) ^ (uint64_t)(t0 + t));
-                e *= 1.0 + J->jitter_rel * (2.0 * ((double)(h >> 11) * 0x1p-53) - 1.0);
-            }
+#ifdef ORACLE_TEST_PLANTS
+            if (J->jitter_rel != 0.0)
+                e *= planted_exp2_error(J, flat, t0 + t);
+#endif
             P[t] = (float)e;
             psum += P[t];
         }
@@ -266,8 +280,8 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
             back = J->k0 - kj;
         }
 
-        /* P-cast: P_fp8 = cast_E4M3(P * Sj); the P-underflow diagnostic counts
-         * zero codes per key category; the decoded value goes back to S units */
+        /* the cast: E4M3 code of P * Sj; zero codes are counted per key
+         * category (Prop. 1); the decoded value goes back to S units */
         for (int t = 0; t < nt; t++) {
             const float y = P[t] * Sj;
             F[t] = 0.0f;
@@ -294,7 +308,8 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
             }
         }
 
-        /* O <- alpha*O + P_fp8 . V_j (FP32 accumulator) */
+        /* the accumulator takes the cast values (Sec. 6.1): FP32 sum of this
+         * block's P~ v, added to the rescaled old accumulator */
         for (int i = 0; i < d; i++)
             blk[i] = 0.0f;
         for (int t = 0; t < nt; t++) {
@@ -321,7 +336,8 @@ static void attn_row(const attn_job* J, int64_t flat, float* out_row,
         mc = mc_new;
     }
 
-    /* epilogue: O / (S * l); lse is the natural-log log-sum-exp of z */
+    /* the output divides by S and by the pre-cast sum; lse is the
+     * natural-log log-sum-exp of z */
     const float denom = S * ell;
     for (int i = 0; i < d; i++)
         out_row[i] = o[i] / denom * J->v_descale;
@@ -406,9 +422,10 @@ static int run_threads(void* (*fn)(void*), void* job, pthread_mutex_t* lock,
  *   unless y lies within amb_rel of a midpoint), it runs the same recurrence
  *   as O over F |V| and takes the same epilogue.  Both ends come from the
  *   cast above, which is monotone in y.
- *   jitter_rel: test use only (planting an exp2 error to check amb against);
- *   when nonzero each exp2 of a P value is multiplied by 1 + jitter_rel * u,
- *   u in [-1, 1) a fixed hash of (row, key).  0 for the method itself.
+ *   jitter_rel: must be 0, except in the test build compiled with
+ *   -DORACLE_TEST_PLANTS, where each exp2 of a P value is multiplied by
+ *   1 + jitter_rel * u, u in [-1, 1) a fixed hash of (row, key), to check
+ *   amb against a known perturbation.
  *   gap_hist, blk_zero, nbins: the per-block diagnostic (both nullable, both
  *   or neither; 1 <= nbins <= 64), accumulated over the given rows and zeroed
  *   here first.  gap_hist[bh][j][bin] counts the rows that visit block j
@@ -433,6 +450,10 @@ int oracle_attn_full(const float* q, const float* k, const float* v, float* out,
         return -1;
     if (!(amb_rel >= 0.0) || !(amb_rel < 0.5) || !(fabs(jitter_rel) < 0.5))
         return -1;
+#ifndef ORACLE_TEST_PLANTS
+    if (jitter_rel != 0.0)
+        return -1;              /* the plant exists only in the test build */
+#endif
     if ((gap_hist != NULL) != (blk_zero != NULL) || (gap_hist && (nbins < 1 || nbins > 64)))
         return -1;
     if (!q || !k || !v || !out || B < 1 || Hq < 1 || Hkv < 1 || N < 1 ||
@@ -478,55 +499,6 @@ int oracle_attn_full(const float* q, const float* k, const float* v, float* out,
     }
     run_threads(attn_worker, &J, &J.lock, nthreads);
     return 0;
-}
-
-int oracle_attn_diag(const float* q, const float* k, const float* v, float* out,
-                     float* lse, uint32_t* counts, float* amb, uint32_t* gap_hist,
-                     uint32_t* blk_zero, int nbins, int B, int Hq, int Hkv, int N, int d,
-                     int causal, int block_kv, int order, float S, int cast, int scale_mode,
-                     int n_sink, float q_descale, float k_descale, float v_descale,
-                     double amb_rel, double jitter_rel, const int64_t* rows, int64_t n_rows,
-                     int nthreads)
-{
-    return oracle_attn_full(q, k, v, out, lse, counts, amb, gap_hist, blk_zero, nbins, B, Hq,
-                            Hkv, N, N, d, causal, block_kv, order, S, cast, scale_mode, n_sink,
-                            q_descale, k_descale, v_descale, amb_rel, jitter_rel, rows, n_rows,
-                            nthreads);
-}
-
-int oracle_attn_bound(const float* q, const float* k, const float* v, float* out,
-                      float* lse, uint32_t* counts, float* amb, int B, int Hq, int Hkv,
-                      int N, int d, int causal, int block_kv, int order, float S, int cast,
-                      int scale_mode, int n_sink, float q_descale, float k_descale,
-                      float v_descale, double amb_rel, double jitter_rel,
-                      const int64_t* rows, int64_t n_rows, int nthreads)
-{
-    return oracle_attn_diag(q, k, v, out, lse, counts, amb, NULL, NULL, 0, B, Hq, Hkv, N, d,
-                            causal, block_kv, order, S, cast, scale_mode, n_sink, q_descale,
-                            k_descale, v_descale, amb_rel, jitter_rel, rows, n_rows, nthreads);
-}
-
-int oracle_attn_descaled(const float* q, const float* k, const float* v, float* out,
-                         float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
-                         int d, int causal, int block_kv, int order, float S, int cast,
-                         int scale_mode, int n_sink, float q_descale, float k_descale,
-                         float v_descale, const int64_t* rows, int64_t n_rows,
-                         int nthreads)
-{
-    return oracle_attn_bound(q, k, v, out, lse, counts, NULL, B, Hq, Hkv, N, d, causal,
-                             block_kv, order, S, cast, scale_mode, n_sink, q_descale,
-                             k_descale, v_descale, 0.0, 0.0, rows, n_rows, nthreads);
-}
-
-int oracle_attn(const float* q, const float* k, const float* v, float* out,
-                float* lse, uint32_t* counts, int B, int Hq, int Hkv, int N,
-                int d, int causal, int block_kv, int order, float S, int cast,
-                int scale_mode, int n_sink, const int64_t* rows, int64_t n_rows,
-                int nthreads)
-{
-    return oracle_attn_descaled(q, k, v, out, lse, counts, B, Hq, Hkv, N, d, causal,
-                                block_kv, order, S, cast, scale_mode, n_sink, 1.0f, 1.0f,
-                                1.0f, rows, n_rows, nthreads);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -620,25 +592,6 @@ int oracle_ref_fp64_kv(const float* q, const float* k, const float* v, double* o
     J.v_descale = v_descale;
     run_threads(ref_worker, &J, &J.lock, nthreads);
     return 0;
-}
-
-int oracle_ref_fp64_descaled(const float* q, const float* k, const float* v,
-                             double* out, double* lse, int B, int Hq, int Hkv, int N,
-                             int d, int causal, double q_descale, double k_descale,
-                             double v_descale, const int64_t* rows, int64_t n_rows,
-                             int nthreads)
-{
-    return oracle_ref_fp64_kv(q, k, v, out, lse, B, Hq, Hkv, N, N, d, causal, q_descale,
-                              k_descale, v_descale, rows, n_rows, nthreads);
-}
-
-int oracle_ref_fp64(const float* q, const float* k, const float* v,
-                    double* out, double* lse, int B, int Hq, int Hkv, int N,
-                    int d, int causal, const int64_t* rows, int64_t n_rows,
-                    int nthreads)
-{
-    return oracle_ref_fp64_descaled(q, k, v, out, lse, B, Hq, Hkv, N, d, causal, 1.0, 1.0,
-                                    1.0, rows, n_rows, nthreads);
 }
 
 int oracle_version(void) { return ORACLE_VERSION; }

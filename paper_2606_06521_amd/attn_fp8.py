@@ -31,7 +31,7 @@ if not os.path.exists(LIB_PATH):
                       "(hipcc --offload-arch=gfx950)")
 _lib = ctypes.CDLL(LIB_PATH)
 
-_P, _I, _F = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+_P, _I, _F, _Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 _lib.attn_fp8_fwd.argtypes = [_P, _P, _P, _P, _P] + [_I] * 8 + [_F, _I, _P]
 _lib.attn_fp8_fwd.restype = _I
 _lib.attn_fp8_p_underflow_count.argtypes = [_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _P, _P, _P, _P]
@@ -41,11 +41,13 @@ _lib.attn_fp8_fwd_descaled.restype = _I
 _lib.attn_fp8_p_underflow_count_descaled.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I]
                                                      + [_F, _F, _F, _P, _P, _P, _P])
 _lib.attn_fp8_p_underflow_count_descaled.restype = _I
-_lib.attn_fp8_fwd_kv.argtypes = [_P] * 5 + [_I] * 9 + [_F, _I, _F, _F, _F, _P]
+_lib.attn_fp8_fwd_kv.argtypes = [_P] * 5 + [_I] * 9 + [_F, _I, _F, _F, _F, _P, _Z, _P]
 _lib.attn_fp8_fwd_kv.restype = _I
 _lib.attn_fp8_p_underflow_count_kv.argtypes = ([_P] * 3 + [_I] * 9 + [_F, _I, _I, _F, _F, _F]
-                                               + [_P] * 4)
+                                               + [_P] * 4 + [_Z, _P])
 _lib.attn_fp8_p_underflow_count_kv.restype = _I
+_lib.attn_fp8_kv_workspace_bytes.argtypes = [_I] * 9 + [ctypes.POINTER(_Z)]
+_lib.attn_fp8_kv_workspace_bytes.restype = _I
 _lib.attn_fp8_block_gap_diag.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _F, _F, _F, _I]
                                          + [_P] * 5 + [_P])
 _lib.attn_fp8_block_gap_diag.restype = _I
@@ -91,19 +93,27 @@ def attn_fp8_p_underflow_count_descaled(q, k, v, B, Hq, Hkv, N, d, causal, block
 
 
 def attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S, mode,
-                    q_descale, k_descale, v_descale, stream):
+                    q_descale, k_descale, v_descale, workspace, workspace_bytes, stream):
     return _lib.attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
                                 float(S), mode, float(q_descale), float(k_descale),
-                                float(v_descale), stream)
+                                float(v_descale), workspace, workspace_bytes, stream)
 
 
 def attn_fp8_p_underflow_count_kv(q, k, v, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S,
                                   mode, n_sink, q_descale, k_descale, v_descale, counts, out,
-                                  lse, stream):
+                                  lse, workspace, workspace_bytes, stream):
     return _lib.attn_fp8_p_underflow_count_kv(q, k, v, B, Hq, Hkv, Nq, Nk, d, causal, block_kv,
                                               order, float(S), mode, n_sink, float(q_descale),
                                               float(k_descale), float(v_descale), counts, out,
-                                              lse, stream)
+                                              lse, workspace, workspace_bytes, stream)
+
+
+def attn_fp8_kv_workspace_bytes(B, Hq, Hkv, Nq, Nk, d, causal, block_kv, mode):
+    """Returns (status, bytes)."""
+    n = _Z(0)
+    st = _lib.attn_fp8_kv_workspace_bytes(B, Hq, Hkv, Nq, Nk, d, causal, block_kv, mode,
+                                          ctypes.byref(n))
+    return st, n.value
 
 
 def attn_fp8_block_gap_diag(q, k, v, B, Hq, Hkv, N, d, causal, block_kv, order, S, mode, n_sink,
@@ -158,12 +168,23 @@ def _stream(stream):
     return s.cuda_stream
 
 
+def kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, mode, device):
+    """A device workspace (torch-allocated) for a KV-cache call of this shape,
+    or None when the call does not split."""
+    st, n = attn_fp8_kv_workspace_bytes(B, Hq, Hkv, N, Nk, d, int(bool(causal)), int(block_kv),
+                                        mode)
+    if st != ATTN_OK:
+        raise AttnError(st)
+    return torch.empty(n, dtype=torch.uint8, device=device) if n else None
+
+
 def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
         block_kv: int = 128, mode: str = "fast", out=None, lse=None, want_lse: bool = True,
         stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
     """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None).
     k, v may hold more keys than q has rows (a KV cache): query row r then
-    sits at key position Nk - N + r.
+    sits at key position Nk - N + r; the call's workspace, if it splits, is
+    taken from torch's allocator on q's device.
     scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8);
     descales = per-tensor (q, k, v) descales of the stored values."""
     m = MODES[mode]
@@ -172,9 +193,10 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
         out = torch.empty((B, Hq, N, d), dtype=torch.float32, device=q.device)
     if lse is None and want_lse:
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
+    ws = kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, m, q.device) if Nk != N else None
     st = attn_fp8_fwd_kv(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N, Nk, d,
                          int(bool(causal)), int(block_kv), ORDERS[order], S, m | SCALES[scale],
-                         *descales, _stream(stream))
+                         *descales, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return out, lse
@@ -187,10 +209,12 @@ def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", caus
     m = MODES[mode]
     B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
     counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
+    ws = kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, m, q.device) if Nk != N else None
     st = attn_fp8_p_underflow_count_kv(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, Nk, d,
                                        int(bool(causal)), int(block_kv), ORDERS[order], S,
                                        m | SCALES[scale], int(n_sink), *descales, _ptr(counts),
-                                       _ptr(out), _ptr(lse), _stream(stream))
+                                       _ptr(out), _ptr(lse), _ptr(ws),
+                                       0 if ws is None else ws.numel(), _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return counts

@@ -1,8 +1,7 @@
 // C ABI of libattn_fp8.so (declared in include/attn_fp8.h): argument
 // validation, choice of kernel instantiation, grid sizing, launch on the
-// caller's stream.  No per-call state is kept; the only memory taken is the
-// prefill kernel's split workspace, one per (device, stream), allocated in
-// stream order on first use and kept until the process ends.
+// caller's stream.  No state is kept and no memory is allocated: the one
+// scratch buffer (the KV-cache split's workspace) is the caller's.
 #include "../../include/attn_fp8.h"
 #include "attn_common.hpp"
 #include "attn_launch.hpp"
@@ -12,7 +11,7 @@
 
 namespace {
 
-constexpr int kVersion = 510;   // 0.5.1: KV-cache prefill tiles split over workgroups
+constexpr int kVersion = 600;   // 0.6.0: the KV-cache split takes the caller's workspace
 
 // Clears the diagnostic's output arrays on the caller's stream (a kernel, not
 // a memset node, so the call stays safe inside a captured graph).
@@ -30,13 +29,18 @@ bool is_pow2_scale(float S)
     return m == 0.5f;
 }
 
-// Shared validation and dispatch of both entry points.
+// One validated call: the launch parameters and the choice of kernel.
+struct Call {
+    attn::Params p;
+    int d, block_kv, mode;
+    bool causal, count, dyn, fast, prefill, empty;
+};
+
+// Validation of everything but the pointers, and the launch parameters.
 // N: query rows, Nk: cached keys (N for self-attention; N <= Nk, row r at key r + Nk - N)
-int run(const void* q, const void* k, const void* v, float* out, float* lse,
-        uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, int causal,
-        int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
-        float k_descale, float v_descale, void* stream, uint32_t* gap_hist = nullptr,
-        uint32_t* blk_zero = nullptr, int nbins = 0)
+int prepare(Call& cl, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, int causal,
+            int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
+            float k_descale, float v_descale)
 {
     const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
     const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
@@ -54,7 +58,11 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         return ATTN_ERR_INVALID_ARG;
     if (!(S > 0.0f) || !isfinite(S))
         return ATTN_ERR_INVALID_ARG;
-    if (n_sink < 0)
+    if (d < 1 || block_kv < 1)
+        return ATTN_ERR_INVALID_ARG;
+    // the count categories (sink keys, the rest of the sink's block, the
+    // other blocks) are disjoint only while the sink keys fit in block 0
+    if (n_sink < 0 || n_sink > block_kv)
         return ATTN_ERR_INVALID_ARG;
     // the dynamic scale keeps S = 2^k0 as its floor, 0 <= k0 <= 8
     int k0 = 0;
@@ -65,52 +73,35 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
         if (f != 0.5f || k0 < 0 || k0 > 8)
             return ATTN_ERR_INVALID_ARG;
     }
-    if (d < 1 || block_kv < 1)
-        return ATTN_ERR_INVALID_ARG;
     if (d != 64 && d != 128)
         return ATTN_ERR_UNSUPPORTED;
     if (block_kv != 64 && block_kv != 128)
         return ATTN_ERR_UNSUPPORTED;
     const int64_t rows = (int64_t)B * Hq * N;
-    if (rows == 0)
-        return ATTN_OK;
-    if (!q || !k || !v)
-        return ATTN_ERR_INVALID_ARG;
-    if (count ? !counts : !out)
-        return ATTN_ERR_INVALID_ARG;
-    // the kernels move q, k, v and out in 16-byte vectors, lse and counts in
-    // 4-byte words (every row of a contiguous tensor then stays aligned)
-    auto misaligned = [](const void* ptr, uintptr_t a) { return ptr && ((uintptr_t)ptr % a) != 0; };
-    if (misaligned(q, 16) || misaligned(k, 16) || misaligned(v, 16) || misaligned(out, 16) ||
-        misaligned(lse, 4) || misaligned(counts, 4) || misaligned(gap_hist, 4) || misaligned(blk_zero, 4))
-        return ATTN_ERR_INVALID_ARG;
-    if ((gap_hist || blk_zero) && (!count || !gap_hist || !blk_zero || nbins < 1 || nbins > 64))
-        return ATTN_ERR_INVALID_ARG;
-    // element offsets stay within 64-bit; the grid must fit a 1-D launch
-    const bool fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
+    cl.empty = rows == 0;
+    cl.d = d;
+    cl.block_kv = block_kv;
+    cl.mode = mode;
+    cl.causal = causal != 0;
+    cl.count = count;
+    cl.dyn = dyn;
+    cl.fast = mode == ATTN_MODE_FAST || mode == ATTN_MODE_FP8QK;
     // Queries against a longer KV cache (fast modes): long query chunks whose
     // offset Nk - N is a multiple of the block run on the persistent kernel
     // (every 32-row wave then still lies in one block of key positions);
     // short ones, or unaligned offsets, on the prefill kernel, whose waves
     // share a 32-row tile's KV blocks.
-    const bool prefill = fast && Nk != N && (N < 128 || (Nk - N) % block_kv != 0);
-    const int bm = prefill ? attn::prefill_rows_per_wg()
-                           : fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
+    cl.prefill = cl.fast && Nk != N && (N < 128 || (Nk - N) % block_kv != 0);
+    const int bm = cl.prefill ? attn::prefill_rows_per_wg()
+                              : cl.fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
     const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;
     const int64_t total = (int64_t)B * Hq * n_tiles;
+    // element offsets stay within 64-bit; the grid must fit a 1-D launch
     if (total > (int64_t)1 << 30)
         return ATTN_ERR_UNSUPPORTED;
 
-    attn::Params p;
-    p.q = q;
-    p.k = k;
-    p.v = v;
-    p.out = out;
-    p.lse = lse;
-    p.counts = counts;
-    p.gap_hist = gap_hist;
-    p.blk_zero = blk_zero;
-    p.nbins = nbins;
+    attn::Params& p = cl.p;
+    p = attn::Params{};
     p.nblk_all = (int)(((int64_t)Nk + block_kv - 1) / block_kv);
     p.Nk = Nk;
     p.qoff = Nk - N;
@@ -132,47 +123,119 @@ int run(const void* q, const void* k, const void* v, float* out, float* lse,
     p.per_xcd = (int)((total + attn::kNumXcd - 1) / attn::kNumXcd);
     p.pairs = (int)((n_tiles + 1) / 2);
     p.units = (long long)B * Hq * p.pairs;
-
     p.nsplit = 1;
-    p.ws_max = nullptr;
-    p.ws_part = nullptr;
+    return ATTN_OK;
+}
 
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    hipError_t e;
-    int dev = 0, n_cu = 0;
-    if (fast && (hipGetDevice(&dev) != hipSuccess ||
-                 hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess))
+int device_cus(int& n_cu)
+{
+    int dev = 0;
+    n_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
         return ATTN_ERR_HIP;
+    return ATTN_OK;
+}
+
+// Workspace bytes a prepared call can use (the KV-cache split), on n_cu CUs.
+size_t workspace_bytes(const Call& cl, int n_cu)
+{
+    return cl.prefill ? attn::prefill_workspace_bytes(cl.p, cl.d, cl.block_kv, cl.causal, n_cu) : 0;
+}
+
+// Validation of the pointers of a prepared, non-empty call.
+int check_pointers(const Call& cl, const void* q, const void* k, const void* v, const float* out,
+                   const float* lse, const uint32_t* counts, const uint32_t* gap_hist,
+                   const uint32_t* blk_zero, int nbins, const void* ws)
+{
+    if (!q || !k || !v)
+        return ATTN_ERR_INVALID_ARG;
+    if (cl.count ? !counts : !out)
+        return ATTN_ERR_INVALID_ARG;
+    // the kernels move q, k, v and out in 16-byte vectors, lse and counts in
+    // 4-byte words (every row of a contiguous tensor then stays aligned)
+    auto misaligned = [](const void* ptr, uintptr_t a) { return ptr && ((uintptr_t)ptr % a) != 0; };
+    if (misaligned(q, 16) || misaligned(k, 16) || misaligned(v, 16) || misaligned(out, 16) ||
+        misaligned(lse, 4) || misaligned(counts, 4) || misaligned(gap_hist, 4) ||
+        misaligned(blk_zero, 4) || misaligned(ws, 256))
+        return ATTN_ERR_INVALID_ARG;
+    if ((gap_hist || blk_zero) && (!cl.count || !gap_hist || !blk_zero || nbins < 1 || nbins > 64))
+        return ATTN_ERR_INVALID_ARG;
+    return ATTN_OK;
+}
+
+// Enqueues a prepared, validated, non-empty call on stream s.
+int launch(Call& cl, const void* q, const void* k, const void* v, float* out, float* lse,
+           uint32_t* counts, uint32_t* gap_hist, uint32_t* blk_zero, int nbins, void* ws,
+           size_t ws_bytes, int n_cu, hipStream_t s)
+{
+    attn::Params& p = cl.p;
+    p.q = q;
+    p.k = k;
+    p.v = v;
+    p.out = out;
+    p.lse = lse;
+    p.counts = counts;
+    p.gap_hist = gap_hist;
+    p.blk_zero = blk_zero;
+    p.nbins = nbins;
     if (gap_hist) {
-        const int64_t nz = (int64_t)B * Hq * p.nblk_all;
+        const int64_t nz = (int64_t)p.B * p.Hq * p.nblk_all;
         hipLaunchKernelGGL(zero_u32, dim3(1024), dim3(256), 0, s, gap_hist, nz * nbins);
         hipLaunchKernelGGL(zero_u32, dim3(1024), dim3(256), 0, s, blk_zero, nz);
         if (hipGetLastError() != hipSuccess)
             return ATTN_ERR_HIP;
     }
-    if (prefill) {
-        const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
-        const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
-        e = attn::launch_prefill(p, d, block_kv, causal != 0, count, scale,
-                                 mode == ATTN_MODE_FP8QK, n_cu, s);
-    } else if (fast) {
-        // the scaled convert applies 1/S exactly only for S = 2^k, and only
-        // below the E4M3 range limit (it does not saturate)
-        const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
-        const int scale = dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
+    const float S = p.S;
+    hipError_t e;
+    // the scaled convert applies 1/S exactly only for S = 2^k, and only
+    // below the E4M3 range limit (it does not saturate)
+    const bool pow2 = is_pow2_scale(S) && S <= 256.0f;
+    const int scale = cl.dyn ? attn::kScaleDynamic : pow2 ? attn::kScalePow2 : attn::kScaleAny;
+    if (cl.prefill) {
+        e = attn::launch_prefill(p, cl.d, cl.block_kv, cl.causal, cl.count, scale,
+                                 cl.mode == ATTN_MODE_FP8QK, n_cu, ws, ws_bytes, s);
+    } else if (cl.fast) {
         // persistent grid: one workgroup per CU (the LDS footprint admits no
         // second one), 8 XCDs, never more workgroups than work units
         const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
         const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
                                                                             : per_xcd_max;
         const int grid = (int)(per_xcd * attn::kNumXcd);
-        e = mode == ATTN_MODE_FP8QK
-                ? attn::launch_fast_qk8(p, grid, d, block_kv, causal != 0, count, scale, s)
-                : attn::launch_fast(p, grid, d, block_kv, causal != 0, count, scale, s);
+        e = cl.mode == ATTN_MODE_FP8QK
+                ? attn::launch_fast_qk8(p, grid, cl.d, cl.block_kv, cl.causal, cl.count, scale, s)
+                : attn::launch_fast(p, grid, cl.d, cl.block_kv, cl.causal, cl.count, scale, s);
     } else {
-        e = attn::launch_faithful(p, d, block_kv, causal != 0, count, mode == ATTN_MODE_FAITHFUL, dyn, s);
+        e = attn::launch_faithful(p, cl.d, cl.block_kv, cl.causal, cl.count,
+                                  cl.mode == ATTN_MODE_FAITHFUL, cl.dyn, s);
     }
     return e == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
+}
+
+// Shared validation and dispatch of the entry points.  ws: the caller's
+// workspace for the KV-cache split (nullptr: no split); a non-null ws must
+// hold at least the bytes attn_fp8_kv_workspace_bytes reports.
+int run(const void* q, const void* k, const void* v, float* out, float* lse,
+        uint32_t* counts, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, int causal,
+        int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
+        float k_descale, float v_descale, void* stream, uint32_t* gap_hist = nullptr,
+        uint32_t* blk_zero = nullptr, int nbins = 0, void* ws = nullptr, size_t ws_bytes = 0)
+{
+    Call cl;
+    int st = prepare(cl, count, B, Hq, Hkv, N, Nk, d, causal, block_kv, order, S, mode_flags,
+                     n_sink, q_descale, k_descale, v_descale);
+    if (st != ATTN_OK || cl.empty)
+        return st;
+    st = check_pointers(cl, q, k, v, out, lse, counts, gap_hist, blk_zero, nbins, ws);
+    if (st != ATTN_OK)
+        return st;
+    int n_cu = 0;
+    if (cl.fast && (st = device_cus(n_cu)) != ATTN_OK)
+        return st;
+    if (ws && ws_bytes < workspace_bytes(cl, n_cu))
+        return ATTN_ERR_INVALID_ARG;
+    return launch(cl, q, k, v, out, lse, counts, gap_hist, blk_zero, nbins, ws, ws_bytes, n_cu,
+                  static_cast<hipStream_t>(stream));
 }
 
 }  // namespace
@@ -229,23 +292,44 @@ int attn_fp8_block_gap_diag(const void* q, const void* k, const void* v, int B, 
                mode, n_sink, q_descale, k_descale, v_descale, stream, gap_hist, blk_zero, nbins);
 }
 
+int attn_fp8_kv_workspace_bytes(int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                                int block_kv, int mode, size_t* bytes)
+{
+    if (!bytes)
+        return ATTN_ERR_INVALID_ARG;
+    *bytes = 0;
+    Call cl;
+    const int st = prepare(cl, false, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, ATTN_ORDER_FORWARD,
+                           256.0f, mode, 0, 1.0f, 1.0f, 1.0f);
+    if (st != ATTN_OK || cl.empty || !cl.prefill)
+        return st;
+    int n_cu = 0;
+    if (device_cus(n_cu) != ATTN_OK)
+        return ATTN_ERR_HIP;
+    *bytes = workspace_bytes(cl, n_cu);
+    return ATTN_OK;
+}
+
 int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse, int B,
                     int Hq, int Hkv, int Nq, int Nk, int d, int causal, int block_kv, int order,
                     float S, int mode, float q_descale, float k_descale, float v_descale,
-                    void* stream)
+                    void* workspace, size_t workspace_bytes, void* stream)
 {
     return run(q, k, v, out, lse, nullptr, false, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
-               S, mode, 0, q_descale, k_descale, v_descale, stream);
+               S, mode, 0, q_descale, k_descale, v_descale, stream, nullptr, nullptr, 0, workspace,
+               workspace_bytes);
 }
 
 int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, int B, int Hq,
                                   int Hkv, int Nq, int Nk, int d, int causal, int block_kv,
                                   int order, float S, int mode, int n_sink, float q_descale,
                                   float k_descale, float v_descale, uint32_t* counts, float* out,
-                                  float* lse, void* stream)
+                                  float* lse, void* workspace, size_t workspace_bytes,
+                                  void* stream)
 {
     return run(q, k, v, out, lse, counts, true, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
-               S, mode, n_sink, q_descale, k_descale, v_descale, stream);
+               S, mode, n_sink, q_descale, k_descale, v_descale, stream, nullptr, nullptr, 0,
+               workspace, workspace_bytes);
 }
 
 const char* attn_fp8_strerror(int status)
@@ -255,10 +339,12 @@ const char* attn_fp8_strerror(int status)
         return "ok";
     case ATTN_ERR_INVALID_ARG:
         return "invalid argument (null pointer, bad shape, Hq % Hkv != 0, S not finite "
-               "and positive, Nq > Nk, or order/mode/causal/n_sink out of range; the dynamic scale "
+               "and positive, Nq > Nk, or order/mode/causal out of range, n_sink outside "
+               "0..block_kv; the dynamic scale "
                "needs S = 2^k with 0 <= k <= 8; descales must be finite and positive; "
                "the block diagnostic needs all three arrays and 1 <= nbins <= 64; q, k, v and "
-               "out must be 16-byte aligned, lse and counts 4-byte aligned)";
+               "out must be 16-byte aligned, lse and counts 4-byte aligned, a workspace "
+               "256-byte aligned and at least attn_fp8_kv_workspace_bytes long)";
     case ATTN_ERR_UNSUPPORTED:
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:

@@ -20,10 +20,13 @@ int fast_rows_per_wg(int d, int block_kv);
 
 // queries against a longer KV cache (p.Nk > p.N), fast modes: one workgroup
 // per (batch, head, 32-row query tile), or several per tile when the tiles
-// cannot fill n_cu compute units (two launches and a temporary workspace on
-// the stream); sets its own grid, nsplit and workspace fields of p
+// cannot fill n_cu compute units and the caller brings a workspace of at least
+// prefill_workspace_bytes() (three launches on the stream); sets its own grid,
+// nsplit and workspace fields of p
 hipError_t launch_prefill(const Params& p, int d, int block_kv, bool causal, bool count, int scale,
-                          bool qk8, int n_cu, hipStream_t stream);
+                          bool qk8, int n_cu, void* ws, size_t ws_bytes, hipStream_t stream);
+// device workspace the split of launch_prefill needs (0: the tiles run unsplit)
+size_t prefill_workspace_bytes(const Params& p, int d, int block_kv, bool causal, int n_cu);
 int prefill_rows_per_wg();
 
 }  // namespace attn

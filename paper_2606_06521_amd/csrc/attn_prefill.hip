@@ -42,9 +42,7 @@
 #include "attn_launch.hpp"
 
 #include <math.h>
-#include <mutex>
 #include <type_traits>
-#include <vector>
 
 namespace attn {
 
@@ -667,103 +665,73 @@ hipError_t launch_phase(const Params& p, int d, int block_kv, bool causal, bool 
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Split workspaces: one per (device, stream), grown on demand and kept until
-// the process ends.  Calls on one stream run in stream order, so they can
-// share its buffer; calls on different streams never do.  A buffer that must
-// grow is released in stream order (after the work already enqueued on its
-// stream) and a larger one taken the same way.  Taking and releasing a
-// buffer on every call would cost the host ~35 us per call (the stream-ordered
-// release), more than the split kernels themselves on the Exp. 1 shape.
-struct Workspace {
-    int dev;
-    hipStream_t stream;
-    void* ptr;
-    size_t bytes;
+// Tiles (32 query rows of one batch and head) that cannot fill the chip are
+// split over C workgroups each: C = min(n_cu / tiles, blocks / 8, 8), so that
+// every wave range holds at least one KV block.  The split's workspace holds
+// the range maxima (tiles * C * 8 * 32 floats) and, from a 256-byte boundary,
+// each workgroup's partial sum (tiles * C * (32 d + 32) floats).  Every entry
+// a launch reads is written earlier in the same call, so it needs no clearing.
+struct Split {
+    long long C;
+    size_t off_part, bytes;
 };
-std::mutex ws_mutex;
-std::vector<Workspace> ws_cache;
 
-void* split_workspace(hipStream_t stream, size_t bytes)
+Split plan_split(const Params& p, int d, int block_kv, bool causal, int n_cu)
 {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess)
-        return nullptr;
-    std::lock_guard<std::mutex> lock(ws_mutex);
-    Workspace* slot = nullptr;
-    for (Workspace& w : ws_cache)
-        if (w.dev == dev && w.stream == stream)
-            slot = &w;
-    if (slot && slot->bytes >= bytes)
-        return slot->ptr;
-    if (slot) {
-        if (hipFreeAsync(slot->ptr, stream) != hipSuccess)
-            (void)hipGetLastError();
-        slot->ptr = nullptr;
-        slot->bytes = 0;
+    const long long units = (long long)p.B * p.Hq * p.n_tiles;
+    // blocks the last tile visits (no tile visits more)
+    const long long nb_max = causal ? ((long long)p.N - 1 + p.qoff) / block_kv + 1
+                                    : ((long long)p.Nk + block_kv - 1) / block_kv;
+    Split sp{1, 0, 0};
+    if (units < n_cu) {
+        long long C = n_cu / units;
+        if (C > nb_max / kPrefillWaves)
+            C = nb_max / kPrefillWaves;
+        if (C > 8)
+            C = 8;
+        sp.C = C < 1 ? 1 : C;
     }
-    void* ptr = nullptr;
-    if (hipMallocAsync(&ptr, bytes, stream) != hipSuccess) {
-        (void)hipGetLastError();
-        return nullptr;
+    if (sp.C > 1) {
+        const size_t n_max = (size_t)units * sp.C * kPrefillWaves * 32;
+        const size_t n_part = (size_t)units * sp.C * (32 * (size_t)d + 32);
+        sp.off_part = align256(n_max * sizeof(float));
+        sp.bytes = sp.off_part + align256(n_part * sizeof(float));
     }
-    if (slot) {
-        slot->ptr = ptr;
-        slot->bytes = bytes;
-    } else {
-        ws_cache.push_back({dev, stream, ptr, bytes});
-    }
-    return ptr;
+    return sp;
 }
 
 }  // namespace
 
-// Tiles (32 query rows of one batch and head) that cannot fill the chip are
-// split over C workgroups each: C = min(n_cu / tiles, blocks / 8, 8), so that
-// every wave range holds at least one KV block.  The split needs a workspace
-// (range maxima, per-workgroup partial sums): the stream's cached one
-// (split_workspace); if it cannot be had the tile runs unsplit.
+size_t prefill_workspace_bytes(const Params& p, int d, int block_kv, bool causal, int n_cu)
+{
+    return plan_split(p, d, block_kv, causal, n_cu).bytes;
+}
+
+// The split runs when the caller's workspace holds at least
+// prefill_workspace_bytes(); without one (ws == nullptr) the tiles run unsplit
+// (same results, fewer workgroups).
 hipError_t launch_prefill(const Params& p_in, int d, int block_kv, bool causal, bool count, int scale,
-                          bool qk8, int n_cu, hipStream_t stream)
+                          bool qk8, int n_cu, void* ws, size_t ws_bytes, hipStream_t stream)
 {
     Params p = p_in;
     p.nsplit = 1;
     p.ws_max = nullptr;
     p.ws_part = nullptr;
     const long long units = (long long)p.B * p.Hq * p.n_tiles;
-    // blocks the last tile visits (no tile visits more)
-    const long long nb_max = causal ? ((long long)p.N - 1 + p.qoff) / block_kv + 1
-                                    : ((long long)p.Nk + block_kv - 1) / block_kv;
-    long long C = 1;
-    if (units < n_cu) {
-        C = n_cu / units;
-        if (C > nb_max / kPrefillWaves)
-            C = nb_max / kPrefillWaves;
-        if (C > 8)
-            C = 8;
-        if (C < 1)
-            C = 1;
-    }
-    void* ws = nullptr;
-    size_t off_part = 0;
-    if (C > 1) {
-        const size_t n_max = (size_t)units * C * kPrefillWaves * 32;
-        const size_t n_part = (size_t)units * C * (32 * (size_t)d + 32);
-        off_part = align256(n_max * sizeof(float));
-        const size_t bytes = off_part + align256(n_part * sizeof(float));
-        ws = split_workspace(stream, bytes);
-        if (!ws)
-            C = 1;
-    }
-    if (C == 1) {
+    Split sp = plan_split(p, d, block_kv, causal, n_cu);
+    if (sp.C > 1 && (!ws || ws_bytes < sp.bytes))
+        sp.C = 1;
+    if (sp.C == 1) {
         p.total_wg = (int)units;
         p.per_xcd = (int)((units + kNumXcd - 1) / kNumXcd);
         return launch_phase(p, d, block_kv, causal, count, scale, qk8, 0, stream);
     }
+    const long long C = sp.C;
     p.nsplit = (int)C;
     p.total_wg = (int)(units * C);
     p.per_xcd = (int)((units + kNumXcd - 1) / kNumXcd * C);
     p.ws_max = static_cast<float*>(ws);
-    p.ws_part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + off_part);
+    p.ws_part = reinterpret_cast<float*>(static_cast<uint8_t*>(ws) + sp.off_part);
     if (count)
         hipLaunchKernelGGL(prefill_zero, dim3(1024), dim3(256), 0, stream, p.counts,
                            (int64_t)p.B * p.Hq * p.N * 3);

@@ -26,7 +26,7 @@ def declared_functions():
 def test_exports_every_declared_symbol(A):
     names = declared_functions()
     assert names == ["attn_fp8_block_gap_diag", "attn_fp8_fwd", "attn_fp8_fwd_descaled",
-                     "attn_fp8_fwd_kv", "attn_fp8_p_underflow_count",
+                     "attn_fp8_fwd_kv", "attn_fp8_kv_workspace_bytes", "attn_fp8_p_underflow_count",
                      "attn_fp8_p_underflow_count_descaled", "attn_fp8_p_underflow_count_kv",
                      "attn_fp8_strerror", "attn_fp8_version"]
     lib = ctypes.CDLL(A.LIB_PATH)
@@ -95,6 +95,9 @@ def test_count_rejects_bad_arguments(A):
                                             a["lse"], a["stream"])
     assert cnt(counts=None) == -1
     assert cnt(n_sink=-1) == -1
+    # sink keys beyond block 0 would fall in two count categories at once
+    assert cnt(n_sink=64 + 8) == -1
+    assert cnt(n_sink=64 + 8, block_kv=128, N=0, counts=None) == 0
     assert cnt(d=32) == -2
     assert cnt(N=0, counts=None) == 0
 
@@ -154,15 +157,33 @@ def test_kv_entry_points_validate(A):
         a.update(kw)
         return A.attn_fp8_fwd_kv(a["q"], a["k"], a["v"], a["out"], None, a["B"], a["Hq"],
                                  a["Hkv"], a["Nq"], a["Nk"], a["d"], a["causal"], a["block_kv"],
-                                 a["order"], a["S"], a["mode"], 1.0, 1.0, 1.0, None)
+                                 a["order"], a["S"], a["mode"], 1.0, 1.0, 1.0, a.get("ws"),
+                                 a.get("ws_bytes", 0), None)
     assert f(Nq=4097) == -1            # more queries than keys
     assert f(Nk=-1) == -1
     assert f(out=None) == -1
     assert f(d=96) == -2
     assert f(Nq=0, q=None, k=None, v=None, out=None) == 0
+    assert f(ws=FAKE + 16, ws_bytes=1 << 20) == -1     # workspace not 256-byte aligned
     cnt = A.attn_fp8_p_underflow_count_kv(FAKE, FAKE, FAKE, 1, 2, 1, 32, 4096, 128, 1, 128, 1,
-                                          256.0, 1, 4, 1.0, 1.0, 1.0, None, None, None, None)
+                                          256.0, 1, 4, 1.0, 1.0, 1.0, None, None, None, None, 0,
+                                          None)
     assert cnt == -1
+    cnt = A.attn_fp8_p_underflow_count_kv(FAKE, FAKE, FAKE, 1, 2, 1, 32, 4096, 128, 1, 128, 1,
+                                          256.0, 1, 129, 1.0, 1.0, 1.0, FAKE, None, None, None, 0,
+                                          None)
+    assert cnt == -1                   # n_sink > block_kv
+
+
+def test_kv_workspace_query_validates(A):
+    import ctypes
+    assert A._lib.attn_fp8_kv_workspace_bytes(1, 2, 1, 32, 4096, 128, 1, 128, 1, None) == -1
+    assert A.attn_fp8_kv_workspace_bytes(1, 2, 1, 33, 32, 128, 1, 128, 1)[0] == -1   # Nq > Nk
+    assert A.attn_fp8_kv_workspace_bytes(1, 2, 1, 32, 4096, 96, 1, 128, 1)[0] == -2
+    # no split without a kernel that splits: square problems, faithful mode, empty problems
+    assert A.attn_fp8_kv_workspace_bytes(1, 2, 1, 64, 64, 128, 1, 128, 1) == (0, 0)
+    assert A.attn_fp8_kv_workspace_bytes(1, 2, 1, 32, 4096, 128, 1, 128, 0) == (0, 0)
+    assert A.attn_fp8_kv_workspace_bytes(0, 2, 1, 32, 4096, 128, 1, 128, 1) == (0, 0)
 
 
 def test_misaligned_pointers_are_rejected(A):

@@ -144,49 +144,96 @@ def test_square_call_through_kv_entry_is_unchanged():
     o2 = torch.empty_like(o1)
     l2 = torch.empty_like(l1)
     st = A.attn_fp8_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o2.data_ptr(), l2.data_ptr(),
-                           1, 4, 2, 300, 300, 128, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0,
+                           1, 4, 2, 300, 300, 128, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0, None, 0,
                            torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     assert st == 0
     assert torch.equal(o1, o2) and torch.equal(l1, l2)
 
 
-def test_split_workspace_growth_and_streams():
-    # The split prefill keeps one workspace per (device, stream).  A small
-    # split, a larger one (the workspace grows) and the small one again on
-    # one stream; then the two problems enqueued back to back on two streams
-    # (separate workspaces).  Every result equals the oracle.
+def test_split_workspace_is_the_callers():
+    # A split shape through the C ABI: with the caller's workspace (split
+    # launches), without one (NULL: the tiles run unsplit) and with one that
+    # is too small (rejected before any launch).  The workspace starts filled
+    # with NaN bytes: nothing is read before the call writes it.  Both runs
+    # equal the oracle, codes and counts included.
     import torch
     from paper_2606_06521_amd import attn_fp8 as A
-    small = last_queries(make_inputs(1, 2, 1, 2000, 128, fmt="bf16_e4m3", delta=8.0, seed=995), 20)
-    large = last_queries(make_inputs(4, 4, 2, 4096, 128, fmt="bf16_e4m3", delta=8.0, seed=996), 40)
-    dsmall, dlarge = to_device(small), to_device(large)
+    inp = last_queries(make_inputs(2, 4, 2, 3000, 128, fmt="bf16_e4m3", delta=8.0, seed=995), 20)
+    q, k, v = to_device(inp)
+    B, Hq, Hkv, Nq, Nk, d = 2, 4, 2, 20, 3000, 128
+    st, nbytes = A.attn_fp8_kv_workspace_bytes(B, Hq, Hkv, Nq, Nk, d, 1, 128, A.ATTN_MODE_FAST)
+    assert st == 0 and nbytes > 0
+    # square problems and the faithful mode never split
+    assert A.attn_fp8_kv_workspace_bytes(B, Hq, Hkv, Nk, Nk, d, 1, 128, A.ATTN_MODE_FAST) == (0, 0)
+    assert A.attn_fp8_kv_workspace_bytes(B, Hq, Hkv, Nq, Nk, d, 1, 128, A.ATTN_MODE_FAITHFUL) == (0, 0)
+    ws = torch.full((nbytes,), 0xFF, dtype=torch.uint8, device="cuda")
+    sptr = torch.cuda.current_stream().cuda_stream
+    for label, wptr, wbytes in (("with workspace", ws.data_ptr(), nbytes), ("no workspace", None, 0)):
+        o = torch.empty((B, Hq, Nq, d), dtype=torch.float32, device="cuda")
+        l = torch.empty((B, Hq, Nq), dtype=torch.float32, device="cuda")
+        c = torch.empty((B, Hq, Nq, 3), dtype=torch.int32, device="cuda")
+        st = A.attn_fp8_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), l.data_ptr(),
+                               B, Hq, Hkv, Nq, Nk, d, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0, wptr,
+                               wbytes, sptr)
+        assert st == 0, label
+        st = A.attn_fp8_p_underflow_count_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, Hq, Hkv,
+                                             Nq, Nk, d, 1, 128, 1, 256.0, 1, 4, 1.0, 1.0, 1.0,
+                                             c.data_ptr(), None, None, wptr, wbytes, sptr)
+        assert st == 0, label
+        torch.cuda.synchronize()
+        log(f"kv split: {label}")
+        compare(inp, (o.cpu().numpy(), l.cpu().numpy(), c.cpu().numpy().view(np.uint32)), "fast",
+                256.0, "reverse", True, 128, label=label)
+    st = A.attn_fp8_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), None, B, Hq,
+                           Hkv, Nq, Nk, d, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0, ws.data_ptr(),
+                           nbytes - 1, sptr)
+    assert st == A.ATTN_ERR_INVALID_ARG
+    st = A.attn_fp8_fwd_kv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), None, B, Hq,
+                           Hkv, Nq, Nk, d, 1, 128, 1, 256.0, 1, 1.0, 1.0, 1.0,
+                           ws.data_ptr() + 16, nbytes - 16, sptr)
+    assert st == A.ATTN_ERR_INVALID_ARG    # a workspace must be 256-byte aligned
 
-    def run(dev, stream):
-        with torch.cuda.stream(stream):
-            q, k, v = dev
-            o, l = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
-        return o, l
 
-    s0 = torch.cuda.current_stream()
-    outs = [(small, run(dsmall, s0)), (large, run(dlarge, s0)), (small, run(dsmall, s0))]
-    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
-    s1.wait_stream(s0)
-    s2.wait_stream(s0)
-    outs += [(small, run(dsmall, s1)), (large, run(dlarge, s2))]
+def test_split_call_in_a_captured_graph():
+    # A split KV-cache call captured in a HIP graph (its workspace comes from
+    # the graph's own pool) and replayed several times, with eager work and a
+    # synchronisation between replays; every replay equals the eager result
+    # bit for bit, and that result equals the oracle.
+    import torch
+    from paper_2606_06521_amd import attn_fp8 as A
+    inp = last_queries(make_inputs(1, 8, 2, 2600, 128, fmt="bf16_e4m3", delta=8.0, seed=981), 24)
+    q, k, v = to_device(inp)
+    o_eager, l_eager = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128,
+                             mode="fast")
     torch.cuda.synchronize()
-    for i, (inp, (o, l)) in enumerate(outs):
-        label = f"kv split workspace call {i}"
-        log(label)
-        gpu = (o.cpu().numpy(), l.cpu().numpy(), None)
-        compare(inp, gpu, "fast", 256.0, "reverse", True, 128, label=label)
+    compare(inp, (o_eager.cpu().numpy(), l_eager.cpu().numpy(), None), "fast", 256.0, "reverse",
+            True, 128, label="kv split eager")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):           # warm-up on the capture stream
+        A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        o_g, l_g = A.fwd(q, k, v, S=256.0, order="reverse", causal=True, block_kv=128, mode="fast")
+    for i in range(4):
+        o_g.fill_(float("nan"))
+        l_g.fill_(float("nan"))
+        g.replay()
+        other, _ = A.fwd(q, k, v, S=1.0, order="forward", causal=True, block_kv=128, mode="fast")
+        torch.cuda.synchronize()
+        log(f"kv split graph replay {i}")
+        assert torch.equal(o_g, o_eager) and torch.equal(l_g, l_eager), i
+        del other
 
 
 def test_split_workspace_two_host_threads():
     # Two host threads, each on its own stream, enqueue different split
     # problems over and over (ctypes releases the GIL during the calls, so
-    # the workspace cache is entered concurrently); every thread's last
-    # result equals the oracle.
+    # the library is entered concurrently; each call has its own workspace);
+    # every thread's last result equals the oracle.
     import threading
     import torch
     from paper_2606_06521_amd import attn_fp8 as A
