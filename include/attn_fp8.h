@@ -108,7 +108,8 @@ enum {
     ATTN_OK = 0,
     ATTN_ERR_INVALID_ARG = -1, /* null pointer, bad shape, S not finite/positive, ... */
     ATTN_ERR_UNSUPPORTED = -2, /* valid but not built: d or block_kv outside {64,128} */
-    ATTN_ERR_HIP = -3          /* the HIP runtime rejected the launch */
+    ATTN_ERR_HIP = -3,         /* the HIP runtime rejected the launch */
+    ATTN_ERR_SCRATCH = -4      /* attn_fp8_fwd_kv_noalloc: shape needs more than its scratch */
 };
 
 /*
@@ -229,6 +230,26 @@ int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, i
                                   float q_descale, float k_descale, float v_descale,
                                   uint32_t* counts, float* out, float* lse,
                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * attn_fp8_fwd_kv without a workspace argument and without allocating: for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  The KV-cache split
+ * takes its scratch from a fixed device array inside the library instead:
+ * 8 MiB per GPU, created when the library's code is loaded on that GPU and
+ * held until the process ends.  The split never needs more than
+ * CUs * (32 d + 288) * 4 + 512 bytes (4.5 MB on a 256-CU MI355X at d = 128);
+ * a shape that would returns ATTN_ERR_SCRATCH, with nothing launched.  Every
+ * call on one GPU shares that GPU's array: calls that overlap in time on one
+ * GPU (different streams or host threads) race and must be serialised by the
+ * caller.  No call reads scratch contents it did not write itself.  Arguments,
+ * results and other return codes as for attn_fp8_fwd_kv.
+ */
+int attn_fp8_fwd_kv_noalloc(const void* q, const void* k, const void* v, float* out,
+                            float* lse, int B, int Hq, int Hkv, int Nq, int Nk, int d,
+                            int causal, int block_kv, int order, float S, int mode,
+                            float q_descale, float k_descale, float v_descale,
+                            void* stream);
 
 /*
  * Workspace the KV-cache entry points can use for the shape (B, Hq, Hkv, Nq,

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libattn_fp8.so")
 ATTN_MODE_FAITHFUL, ATTN_MODE_FAST, ATTN_MODE_NOCAST, ATTN_MODE_FP8QK = 0, 1, 2, 3
 ATTN_ORDER_FORWARD, ATTN_ORDER_REVERSE = 0, 1
 ATTN_OK, ATTN_ERR_INVALID_ARG, ATTN_ERR_UNSUPPORTED, ATTN_ERR_HIP = 0, -1, -2, -3
+ATTN_ERR_SCRATCH = -4
 ATTN_SCALE_DYNAMIC = 0x100
 
 MODES = {"faithful": ATTN_MODE_FAITHFUL, "fast": ATTN_MODE_FAST, "nocast": ATTN_MODE_NOCAST,
@@ -46,6 +47,8 @@ _lib.attn_fp8_fwd_kv.restype = _I
 _lib.attn_fp8_p_underflow_count_kv.argtypes = ([_P] * 3 + [_I] * 9 + [_F, _I, _I, _F, _F, _F]
                                                + [_P] * 4 + [_Z, _P])
 _lib.attn_fp8_p_underflow_count_kv.restype = _I
+_lib.attn_fp8_fwd_kv_noalloc.argtypes = [_P] * 5 + [_I] * 9 + [_F, _I, _F, _F, _F, _P]
+_lib.attn_fp8_fwd_kv_noalloc.restype = _I
 _lib.attn_fp8_kv_workspace_bytes.argtypes = [_I] * 9 + [ctypes.POINTER(_Z)]
 _lib.attn_fp8_kv_workspace_bytes.restype = _I
 _lib.attn_fp8_block_gap_diag.argtypes = ([_P, _P, _P] + [_I] * 8 + [_F, _I, _I, _F, _F, _F, _I]
@@ -97,6 +100,13 @@ def attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, 
     return _lib.attn_fp8_fwd_kv(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order,
                                 float(S), mode, float(q_descale), float(k_descale),
                                 float(v_descale), workspace, workspace_bytes, stream)
+
+
+def attn_fp8_fwd_kv_noalloc(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S,
+                            mode, q_descale, k_descale, v_descale, stream):
+    return _lib.attn_fp8_fwd_kv_noalloc(q, k, v, out, lse, B, Hq, Hkv, Nq, Nk, d, causal,
+                                        block_kv, order, float(S), mode, float(q_descale),
+                                        float(k_descale), float(v_descale), stream)
 
 
 def attn_fp8_p_underflow_count_kv(q, k, v, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S,

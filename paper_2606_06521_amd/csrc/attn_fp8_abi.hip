@@ -9,9 +9,20 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
+// Scratch of the allocation-free KV-cache entry point (attn_fp8_fwd_kv_noalloc):
+// a file-scope device array, one copy per GPU, resident from the library's
+// load on that GPU until the process ends.  The KV-cache split needs at most
+// CUs * (32 d + 288) * 4 + 512 bytes (4.5 MB on 256 CUs at d = 128).  Host
+// code never names the array in a kernel argument or a copy: it uses the
+// per-device address from hipGetSymbolAddress (scratch_on_device below).
+constexpr size_t kScratchBytes = (size_t)8 << 20;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
 namespace {
 
-constexpr int kVersion = 600;   // 0.6.0: the KV-cache split takes the caller's workspace
+constexpr int kVersion = 610;   // 0.6.1: allocation-free KV-cache entry point
 
 // Clears the diagnostic's output arrays on the caller's stream (a kernel, not
 // a memset node, so the call stays safe inside a captured graph).
@@ -212,6 +223,29 @@ int launch(Call& cl, const void* q, const void* k, const void* v, float* out, fl
     return e == hipSuccess ? ATTN_OK : ATTN_ERR_HIP;
 }
 
+// Device address of `scratch` on the current device, taken once per device
+// (with that device current) and kept; nullptr if the runtime refuses.
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mutex;
+void* scratch_ptr[kMaxDevices];
+
+void* scratch_on_device()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return nullptr;
+    std::lock_guard<std::mutex> lock(scratch_mutex);
+    if (!scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) {
+            (void)hipGetLastError();
+            return nullptr;
+        }
+        scratch_ptr[dev] = ptr;
+    }
+    return scratch_ptr[dev];
+}
+
 // Shared validation and dispatch of the entry points.  ws: the caller's
 // workspace for the KV-cache split (nullptr: no split); a non-null ws must
 // hold at least the bytes attn_fp8_kv_workspace_bytes reports.
@@ -320,6 +354,32 @@ int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, flo
                workspace_bytes);
 }
 
+int attn_fp8_fwd_kv_noalloc(const void* q, const void* k, const void* v, float* out, float* lse,
+                            int B, int Hq, int Hkv, int Nq, int Nk, int d, int causal,
+                            int block_kv, int order, float S, int mode, float q_descale,
+                            float k_descale, float v_descale, void* stream)
+{
+    Call cl;
+    int st = prepare(cl, false, B, Hq, Hkv, Nq, Nk, d, causal, block_kv, order, S, mode, 0,
+                     q_descale, k_descale, v_descale);
+    if (st != ATTN_OK || cl.empty)
+        return st;
+    st = check_pointers(cl, q, k, v, out, lse, nullptr, nullptr, nullptr, 0, nullptr);
+    if (st != ATTN_OK)
+        return st;
+    int n_cu = 0;
+    if (cl.fast && (st = device_cus(n_cu)) != ATTN_OK)
+        return st;
+    const size_t need = workspace_bytes(cl, n_cu);
+    if (need > kScratchBytes)
+        return ATTN_ERR_SCRATCH;
+    void* ws = nullptr;
+    if (need > 0 && !(ws = scratch_on_device()))
+        return ATTN_ERR_HIP;
+    return launch(cl, q, k, v, out, lse, nullptr, nullptr, nullptr, 0, ws, ws ? kScratchBytes : 0,
+                  n_cu, static_cast<hipStream_t>(stream));
+}
+
 int attn_fp8_p_underflow_count_kv(const void* q, const void* k, const void* v, int B, int Hq,
                                   int Hkv, int Nq, int Nk, int d, int causal, int block_kv,
                                   int order, float S, int mode, int n_sink, float q_descale,
@@ -349,6 +409,9 @@ const char* attn_fp8_strerror(int status)
         return "unsupported configuration (d and block_kv must be 64 or 128)";
     case ATTN_ERR_HIP:
         return "the HIP runtime rejected the kernel launch";
+    case ATTN_ERR_SCRATCH:
+        return "the allocation-free entry point's fixed scratch (8 MiB per GPU) is smaller "
+               "than this shape's KV-cache split needs";
     default:
         return "unknown status";
     }

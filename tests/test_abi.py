@@ -26,7 +26,8 @@ def declared_functions():
 def test_exports_every_declared_symbol(A):
     names = declared_functions()
     assert names == ["attn_fp8_block_gap_diag", "attn_fp8_fwd", "attn_fp8_fwd_descaled",
-                     "attn_fp8_fwd_kv", "attn_fp8_kv_workspace_bytes", "attn_fp8_p_underflow_count",
+                     "attn_fp8_fwd_kv", "attn_fp8_fwd_kv_noalloc", "attn_fp8_kv_workspace_bytes",
+                     "attn_fp8_p_underflow_count",
                      "attn_fp8_p_underflow_count_descaled", "attn_fp8_p_underflow_count_kv",
                      "attn_fp8_strerror", "attn_fp8_version"]
     lib = ctypes.CDLL(A.LIB_PATH)
@@ -36,7 +37,8 @@ def test_exports_every_declared_symbol(A):
 
 def test_version_and_strerror(A):
     assert A.attn_fp8_version() >= 100
-    for st in (A.ATTN_OK, A.ATTN_ERR_INVALID_ARG, A.ATTN_ERR_UNSUPPORTED, A.ATTN_ERR_HIP, 12345):
+    for st in (A.ATTN_OK, A.ATTN_ERR_INVALID_ARG, A.ATTN_ERR_UNSUPPORTED, A.ATTN_ERR_HIP,
+               A.ATTN_ERR_SCRATCH, 12345):
         assert isinstance(A.attn_fp8_strerror(st), str) and A.attn_fp8_strerror(st)
 
 
@@ -45,7 +47,7 @@ def test_enum_values_match_header(A):
     for name in ["ATTN_MODE_FAITHFUL", "ATTN_MODE_FAST", "ATTN_MODE_NOCAST", "ATTN_MODE_FP8QK",
                  "ATTN_ORDER_FORWARD",
                  "ATTN_ORDER_REVERSE", "ATTN_OK", "ATTN_ERR_INVALID_ARG", "ATTN_ERR_UNSUPPORTED",
-                 "ATTN_ERR_HIP"]:
+                 "ATTN_ERR_HIP", "ATTN_ERR_SCRATCH"]:
         m = re.search(name + r"\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(A, name), name
     m = re.search(r"ATTN_SCALE_DYNAMIC\s*=\s*(0x[0-9a-fA-F]+)", text)
@@ -173,6 +175,22 @@ def test_kv_entry_points_validate(A):
                                           256.0, 1, 129, 1.0, 1.0, 1.0, FAKE, None, None, None, 0,
                                           None)
     assert cnt == -1                   # n_sink > block_kv
+
+
+def test_noalloc_entry_point_validates(A):
+    def f(**kw):
+        a = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, B=1, Hq=2, Hkv=1, Nq=32, Nk=4096, d=128,
+                 causal=1, block_kv=128, order=1, S=256.0, mode=1)
+        a.update(kw)
+        return A.attn_fp8_fwd_kv_noalloc(a["q"], a["k"], a["v"], a["out"], None, a["B"], a["Hq"],
+                                         a["Hkv"], a["Nq"], a["Nk"], a["d"], a["causal"],
+                                         a["block_kv"], a["order"], a["S"], a["mode"], 1.0, 1.0,
+                                         1.0, None)
+    assert f(Nq=4097) == -1
+    assert f(out=None) == -1
+    assert f(q=FAKE + 8) == -1
+    assert f(d=96) == -2
+    assert f(Nq=0, q=None, k=None, v=None, out=None) == 0
 
 
 def test_kv_workspace_query_validates(A):
