@@ -178,15 +178,13 @@ __device__ inline float halves_sum(float x)
 
 __device__ inline float fmax_f(float a, float b) { return __builtin_fmaxf(a, b); }
 
-// Number of zero bytes in a 32-bit word.
-__device__ inline uint32_t zero_bytes(uint32_t w)
+// Number of zero bytes in a word of four E4M3 codes of non-negative values
+// (every byte <= 0x7F): adding 0x7F to the low seven bits of a byte sets its
+// top bit unless the byte is zero, with no carry into the next byte.
+__device__ inline uint32_t zero_codes(uint32_t w)
 {
-    uint32_t n = 0;
-    n += (w & 0x000000FFu) == 0;
-    n += (w & 0x0000FF00u) == 0;
-    n += (w & 0x00FF0000u) == 0;
-    n += (w & 0xFF000000u) == 0;
-    return n;
+    const uint32_t nz = ((w & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | w;
+    return (uint32_t)__builtin_popcount(~nz & 0x80808080u);
 }
 
 }  // namespace attn

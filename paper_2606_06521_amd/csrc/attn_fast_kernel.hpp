@@ -426,6 +426,9 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             }
             __builtin_amdgcn_sched_barrier(0);
             uint32_t bz = 0;   // zero codes of this block (valid rows and keys)
+            // keys of the sink's block, the diagonal block and a ragged last
+            // block need a validity and category mask per word
+            const bool slow_count = j == 0 || (CAUSAL && j == nblk_w - 1) || t0 + BC > Nk;
             float lpart[KT];
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
@@ -462,21 +465,49 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                         word = (uint32_t)wv;
                     }
                     pk[kt][r4] = word;
-                    if (COUNT) {
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const int key = t0 + 32 * kt + 16 * h + 4 * r4 + i;
-                            const bool z = ((word >> (8 * i)) & 0xFFu) == 0 && key < Nk &&
-                                           (!CAUSAL || key <= row + qoff);
-                            if (z) {
-                                if (j > 0) ++cnt2;
-                                else if (key < p.n_sink) ++cnt0;
-                                else ++cnt1;
-                                bz += row < N;
-                            }
-                        }
-                    }
                 }
+            }
+            // every key of a block past the sink's, off the diagonal and inside
+            // the keys is valid and in category 2: count its zero codes by word
+            if (COUNT && slow_count) {
+                // byte i of word (kt, r4) holds key t0 + o + i, o = 32 kt + 16 h + 4 r4;
+                // it is valid iff o + i <= lim, and a sink key iff o + i < ns
+                const int lim = (CAUSAL ? min(row + qoff, Nk - 1) : Nk - 1) - t0;
+                const int ns = j == 0 ? p.n_sink : 0;
+                auto low_bytes = [](int n) __attribute__((always_inline)) {
+                    const int c = min(max(n, 0), 4);
+                    return (uint32_t)((1ull << (8 * c)) - 1);
+                };
+                uint32_t z0 = 0, zn = 0;
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        const int o = 32 * kt + 16 * h + 4 * r4;
+                        const uint32_t valid = low_bytes(lim - o + 1);
+                        const uint32_t sink = low_bytes(ns - o);
+                        const uint32_t wd = pk[kt][r4];
+                        // invalid or other-category bytes are forced non-zero
+                        z0 += zero_codes(wd | ~(valid & sink));
+                        zn += zero_codes(wd | ~(valid & ~sink));
+                    }
+                if (j > 0) {
+                    cnt2 += zn;
+                } else {
+                    cnt0 += z0;
+                    cnt1 += zn;
+                }
+                bz += row < N ? z0 + zn : 0u;
+            }
+            if (COUNT && !slow_count) {
+                uint32_t zc = 0;
+#pragma unroll
+                for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4)
+                        zc += zero_codes(pk[kt][r4]);
+                cnt2 += zc;
+                bz += row < N ? zc : 0u;
             }
             if (COUNT && p.blk_zero)
                 record_block_zeros(p, bh, j, bz);

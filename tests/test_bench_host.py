@@ -60,3 +60,27 @@ def test_more_than_one_gpu_is_refused_with_a_message():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode != 0
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_report_markdown_and_paper_context(tmp_path):
+    # the report's markdown summary from one synthetic run record, and the
+    # paper context attached only where the paper has a figure for the run
+    import json
+    import bench
+    rec = {"config": "C2", "workload": "w", "mode": "faithful", "S": 1.0, "order": "forward",
+           "delta": 7.0, "delta_eff": 7.0, "gpu_ms_median": 1.0, "timed_launches": 20,
+           "tflops": 68.7, "peak_tflops": 157.3, "frac_of_peak": 0.437,
+           "mse_gpu_vs_fp64": 5.5e-5, "mse_oracle_vs_fp64": 5.5e-5,
+           "max_abs_gpu_minus_oracle": 1e-6, "max_abs_lse_gpu_minus_oracle": 1e-7,
+           "zero_fraction_nonsink": 0.81, "collapse_fraction_F": 0.86,
+           "counts_equal_on_oracle_rows": True,
+           "oracle": {"rows": 8192, "rows_total": 32768, "sample": "every 4th flat row",
+                      "pairs": 1, "seconds": 0.5, "cores": 16, "tflops": 0.1},
+           "paper_context": bench._paper_context("C2", "forward", 1.0, 7.0)}
+    p = tmp_path / "r.jsonl"
+    p.write_text(json.dumps(rec) + "\n")
+    md = open(bench.write_report_md(str(p))).read()
+    assert "| C2 | 7.0 | 1 | forward |" in md
+    assert "table1_frac_zeroed=0.82" in md and "table2_mse=5.65e-05" in md
+    assert bench._paper_context("C2", "reverse", 16.0, 7.0) == {}
+    assert bench._paper_context("C4", "forward", 1.0, 9.0) == {}
