@@ -344,11 +344,13 @@ def cpu_baseline(inp, w, order, S, out_dev, lse_dev, cnt_gpu, sample_rows, out_d
                                                        seed=0)[:64]]))
     keys = (rows % w.rows + (w.N - w.rows) + 1) if w.causal else np.full(rows.size, w.N)
     flops = float(4.0 * w.d * keys.sum())
+    fast = w.mode in ("fast", "fp8qk")
     t0 = time.perf_counter()
-    o_out, o_lse, o_cnt = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order,
-                                      block_kv=w.block_kv, causal=w.causal, n_sink=inp.n_sink,
-                                      rows=rows, nthreads=nthreads)
+    res = oracle.attn(inp.q32, inp.k32, inp.v32, S=S, order=order, block_kv=w.block_kv,
+                      causal=w.causal, n_sink=inp.n_sink, rows=rows, nthreads=nthreads,
+                      bound_rel=6.0 * 2.0 ** -23 if fast else None)
     dt = time.perf_counter() - t0
+    o_out, o_lse, o_cnt = res[:3]
     ref, _ = oracle.ref_fp64(inp.q32, inp.k32, inp.v32, causal=w.causal, rows=rows, nthreads=nthreads)
     g = out_dev.cpu().numpy().reshape(-1, w.d)[rows]
     mse_gpu = float(np.mean((g.astype(np.float64) - ref) ** 2))
@@ -363,6 +365,12 @@ def cpu_baseline(inp, w, order, S, out_dev, lse_dev, cnt_gpu, sample_rows, out_d
             for i, (name, n) in enumerate((("sink", n_s), ("sink_block_nonsink", n_b0),
                                            ("other_blocks", n_o)))}
     extra = {}
+    if fast:
+        # elements past the spec bar (2e-2), and past it plus the
+        # per-element code-ambiguity bound the parity tests allow
+        diff = np.abs(g.astype(np.float64) - o_out)
+        extra["n_out_past_2e-2"] = int((diff > 2e-2).sum())
+        extra["n_out_past_2e-2_plus_amb"] = int((diff > 2e-2 + res[3]).sum())
     if out_dyn_dev is not None:
         gd = out_dyn_dev.cpu().numpy().reshape(-1, w.d)[rows]
         extra["mse_gpu_dynamic_scale_vs_fp64"] = float(np.mean((gd.astype(np.float64) - ref) ** 2))
