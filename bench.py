@@ -37,8 +37,11 @@ DTYPES = {"fast": "bf16 QK^T + e4m3 P.V, fp32 accumulate",
           "fp8qk": "e4m3 QK^T + e4m3 P.V, fp32 accumulate",
           "faithful": "fp32", "nocast": "fp32"}
 KERNEL_SOURCES = ["paper_2606_06521_amd/csrc/attn_fast_kernel.hpp",
+                  "paper_2606_06521_amd/csrc/attn_fast_dispatch.hpp",
                   "paper_2606_06521_amd/csrc/attn_fast.hip",
+                  "paper_2606_06521_amd/csrc/attn_fast_pair.hip",
                   "paper_2606_06521_amd/csrc/attn_fast_qk8.hip",
+                  "paper_2606_06521_amd/csrc/attn_fast_qk8_pair.hip",
                   "paper_2606_06521_amd/csrc/attn_prefill.hip",
                   "paper_2606_06521_amd/csrc/attn_common.hpp"]
 HBM_PEAK_GBS = 8000.0

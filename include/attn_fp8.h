@@ -99,6 +99,24 @@ enum {
  */
 enum { ATTN_SCALE_DYNAMIC = 0x100 };
 
+/*
+ * Flags OR-ed into `mode` (fast modes, self-attention and long query chunks
+ * of a KV cache): the schedule of the persistent kernel.
+ *   ATTN_TILE_256  256 query rows per tile, eight waves of 32 rows, every
+ *                  wave over every KV block of its rows; tiles t and T-1-t of
+ *                  a head form one work unit (equal causal work per unit).
+ *   ATTN_TILE_128  128 query rows per tile, one tile per work unit; the two
+ *                  waves of a 32-row group take alternate KV blocks of the
+ *                  visit and hand the running maximum to each other, so every
+ *                  block still sees the running maximum of Algorithm 1.
+ * Neither: ATTN_TILE_256 unless its units would leave at least half of the
+ * GPU's compute units idle.  Both: ATTN_ERR_INVALID_ARG.  The two schedules
+ * give identical E4M3 codes and counts; O and l differ only in FP32 rounding
+ * (each 128-row group adds two partial sums at the end).  No effect in the
+ * other modes or on short query chunks.
+ */
+enum { ATTN_TILE_256 = 0x200, ATTN_TILE_128 = 0x400 };
+
 enum {
     ATTN_ORDER_FORWARD = 0, /* KV blocks 0, 1, ..., last (sink block first)  */
     ATTN_ORDER_REVERSE = 1  /* KV blocks last, ..., 1, 0 (sink block last)   */
@@ -127,7 +145,7 @@ enum {
  *   order     ATTN_ORDER_FORWARD or ATTN_ORDER_REVERSE.
  *   S         static P-scale (Sec. 5), finite and > 0.  Powers of two make the
  *             scaling exact (Prop. 2); S = 256 is the paper's choice.
- *   mode      ATTN_MODE_*, optionally OR ATTN_SCALE_DYNAMIC.
+ *   mode      ATTN_MODE_*, optionally OR ATTN_SCALE_DYNAMIC and one ATTN_TILE_*.
  *   stream    hipStream_t or NULL.
  * Returns ATTN_OK or an ATTN_ERR_* code.
  */

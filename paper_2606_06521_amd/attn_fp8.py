@@ -21,11 +21,13 @@ ATTN_ORDER_FORWARD, ATTN_ORDER_REVERSE = 0, 1
 ATTN_OK, ATTN_ERR_INVALID_ARG, ATTN_ERR_UNSUPPORTED, ATTN_ERR_HIP = 0, -1, -2, -3
 ATTN_ERR_SCRATCH = -4
 ATTN_SCALE_DYNAMIC = 0x100
+ATTN_TILE_256, ATTN_TILE_128 = 0x200, 0x400
 
 MODES = {"faithful": ATTN_MODE_FAITHFUL, "fast": ATTN_MODE_FAST, "nocast": ATTN_MODE_NOCAST,
          "fp8qk": ATTN_MODE_FP8QK}
 ORDERS = {"forward": ATTN_ORDER_FORWARD, "reverse": ATTN_ORDER_REVERSE}
 SCALES = {"static": 0, "dynamic": ATTN_SCALE_DYNAMIC}
+TILES = {None: 0, 256: ATTN_TILE_256, 128: ATTN_TILE_128}   # fast kernel schedule (None: automatic)
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
@@ -190,13 +192,14 @@ def kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, mode, device):
 
 def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
         block_kv: int = 128, mode: str = "fast", out=None, lse=None, want_lse: bool = True,
-        stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
+        stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0), tile=None):
     """Attention forward; returns (out [B,Hq,N,d] float32, lse [B,Hq,N] float32 or None).
     k, v may hold more keys than q has rows (a KV cache): query row r then
     sits at key position Nk - N + r; the call's workspace, if it splits, is
     taken from torch's allocator on q's device.
     scale="dynamic" ORs ATTN_SCALE_DYNAMIC into the mode (S = 2^k0, k0 <= 8);
-    descales = per-tensor (q, k, v) descales of the stored values."""
+    descales = per-tensor (q, k, v) descales of the stored values; tile = 256 or
+    128 forces the fast kernel's schedule (ATTN_TILE_*), None lets the library pick."""
     m = MODES[mode]
     B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
     if out is None:
@@ -205,8 +208,9 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
         lse = torch.empty((B, Hq, N), dtype=torch.float32, device=q.device)
     ws = kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, m, q.device) if Nk != N else None
     st = attn_fp8_fwd_kv(_ptr(q), _ptr(k), _ptr(v), _ptr(out), _ptr(lse), B, Hq, Hkv, N, Nk, d,
-                         int(bool(causal)), int(block_kv), ORDERS[order], S, m | SCALES[scale],
-                         *descales, _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream))
+                         int(bool(causal)), int(block_kv), ORDERS[order], S,
+                         m | SCALES[scale] | TILES[tile], *descales, _ptr(ws),
+                         0 if ws is None else ws.numel(), _stream(stream))
     if st != ATTN_OK:
         raise AttnError(st)
     return out, lse
@@ -214,7 +218,7 @@ def fwd(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = Fal
 
 def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
                       block_kv: int = 128, mode: str = "fast", n_sink: int = 4, out=None, lse=None,
-                      stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
+                      stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0), tile=None):
     """P-underflow diagnostic; returns counts [B,Hq,N,3] uint32 (as int32 storage)."""
     m = MODES[mode]
     B, Hq, Hkv, N, d, Nk = _check(q, k, v, m)
@@ -222,7 +226,8 @@ def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", caus
     ws = kv_workspace(B, Hq, Hkv, N, Nk, d, causal, block_kv, m, q.device) if Nk != N else None
     st = attn_fp8_p_underflow_count_kv(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, Nk, d,
                                        int(bool(causal)), int(block_kv), ORDERS[order], S,
-                                       m | SCALES[scale], int(n_sink), *descales, _ptr(counts),
+                                       m | SCALES[scale] | TILES[tile], int(n_sink), *descales,
+                                       _ptr(counts),
                                        _ptr(out), _ptr(lse), _ptr(ws),
                                        0 if ws is None else ws.numel(), _stream(stream))
     if st != ATTN_OK:
@@ -232,7 +237,7 @@ def p_underflow_count(q, k, v, *, S: float = 256.0, order: str = "reverse", caus
 
 def block_gap_diag(q, k, v, *, S: float = 256.0, order: str = "reverse", causal: bool = False,
                    block_kv: int = 128, mode: str = "fast", n_sink: int = 4, nbins: int = 32,
-                   stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0)):
+                   stream=None, scale: str = "static", descales=(1.0, 1.0, 1.0), tile=None):
     """Per-block diagnostic; returns (gap_hist [B,Hq,nblk,nbins], blk_zero [B,Hq,nblk],
     counts [B,Hq,N,3]), all uint32 held in int32 storage."""
     m = MODES[mode]
@@ -244,7 +249,8 @@ def block_gap_diag(q, k, v, *, S: float = 256.0, order: str = "reverse", causal:
     bz = torch.empty((B, Hq, nblk), dtype=torch.int32, device=q.device)
     counts = torch.empty((B, Hq, N, 3), dtype=torch.int32, device=q.device)
     st = attn_fp8_block_gap_diag(_ptr(q), _ptr(k), _ptr(v), B, Hq, Hkv, N, d, int(bool(causal)),
-                                 int(block_kv), ORDERS[order], S, m | SCALES[scale], int(n_sink),
+                                 int(block_kv), ORDERS[order], S, m | SCALES[scale] | TILES[tile],
+                                 int(n_sink),
                                  *descales, int(nbins), _ptr(hist), _ptr(bz), _ptr(counts), None,
                                  None, _stream(stream))
     if st != ATTN_OK:

@@ -16,8 +16,8 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libattn_fp8.so")
 
-SOURCES = ["attn_fp8_abi.hip", "attn_fast.hip", "attn_fast_qk8.hip", "attn_faithful.hip",
-           "attn_prefill.hip"]
+SOURCES = ["attn_fp8_abi.hip", "attn_fast.hip", "attn_fast_pair.hip", "attn_fast_qk8.hip",
+           "attn_fast_qk8_pair.hip", "attn_faithful.hip", "attn_prefill.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # -packed-fp32-ops: no packed FP32 VALU instructions anywhere in the device code

@@ -58,18 +58,49 @@ typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
 // the next barrier; the kernel waits for it explicitly (wait_loads) before
 // the barrier that publishes the stage.  M0 holds the wave's LDS base and is
 // used by nothing else in this kernel.
-__device__ inline void g2lds16(const uint8_t* base, uint32_t voff, const uint8_t* dst_wave_base)
+__device__ inline void g2lds16(const uint8_t* base, uint32_t voff, uint32_t lds)
 {
-    const uint32_t lds = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)dst_wave_base;
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
                  :
                  : "s"(__builtin_amdgcn_readfirstlane(lds)), "v"(voff), "s"(base)
                  : "memory");
 }
 
+// LDS byte address of a pointer into a __shared__ array, or of an LDS address
+// already in hand (the 128-row schedule computes its stage addresses so)
+__device__ inline uint32_t lds_addr(const uint8_t* p)
+{
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)p;
+}
+__device__ inline uint32_t lds_addr(uint32_t a) { return a; }
+
+__device__ inline void g2lds16(const uint8_t* base, uint32_t voff, const uint8_t* dst_wave_base)
+{
+    g2lds16(base, voff, lds_addr(dst_wave_base));
+}
+
 __device__ inline void wait_loads()
 {
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// LDS load from an integer LDS address
+template <typename T>
+__device__ inline T lds_load(uint32_t a)
+{
+    return *reinterpret_cast<const __attribute__((address_space(3))) T*>((uintptr_t)a);
+}
+
+// Materialises a per-lane LDS address in one register: the loads that share
+// it then carry their constant offsets in the instruction (the 128-row
+// schedule's stages move from block to block, so the compiler would otherwise
+// keep a register per address and add the stage to each).  Applied to a lane
+// offset it also keeps the compiler from hoisting the offset's XOR variants
+// out of the loop into registers of their own.
+__device__ inline uint32_t lds_base(uint32_t a)
+{
+    asm volatile("" : "+v"(a));
+    return a;
 }
 
 __device__ inline i32x2 lds_read_tr8(const uint8_t* p)
@@ -81,11 +112,20 @@ __device__ inline i32x2 lds_read_tr8(const uint8_t* p)
 
 // SCALE: kScaleAny (static S, multiply and convert), kScalePow2 (static
 // S = 2^k, the scaled convert) or kScaleDynamic (per-block 2^kj, see softmax).
-template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8>
+// PAIR: the 128-row schedule.  Waves w and w + 4 (one per group, on one SIMD)
+// share a 32-row group and take alternate blocks of the visit: group g the
+// blocks at visit positions k = g, g + 2, ...  The running maximum after
+// each block is handed to the partner through LDS, so every block still sees
+// the running maximum of the sequential visit (P, its E4M3 code and the counts
+// are those of the 256-row schedule); each wave keeps its own (O, l), brought
+// to the row's final maximum and added at the end of the tile.  Each tile is
+// one work unit (no pairing), which fills the chip when 256-row tiles leave
+// CUs idle.
+template <int D, int BC, bool CAUSAL, bool COUNT, int SCALE, bool QK8, bool PAIR>
 __global__ void __launch_bounds__(512) fast_kernel(Params p)
 {
     constexpr int NW = 8;
-    constexpr int BM = 32 * NW;
+    constexpr int BM = PAIR ? 32 * (NW / 2) : 32 * NW;
     constexpr int KT = BC / 32;                 // 32-key S^T tiles per block
     constexpr int DK = QK8 ? D / 64 : D / 16;   // S^T MFMA k-steps over d
     constexpr int DT = D / 32;                  // 32-wide d tiles of O^T
@@ -102,10 +142,16 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     constexpr int V_NI = V_BYTES / 4096;
     static_assert(K_NI >= 1 && V_NI >= 1, "stage smaller than one round of loads");
 
-    __shared__ __attribute__((aligned(1024))) uint8_t Ks0[K_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Ks1[K_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Vs0[V_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Vs1[V_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks0[PAIR ? 1 : K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Ks1[PAIR ? 1 : K_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs0[PAIR ? 1 : V_BYTES];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vs1[PAIR ? 1 : V_BYTES];
+    // PAIR: two K and two V stages (stage r at Kst + r K_BYTES, Vst +
+    // r V_BYTES), and the running maximum of each row (row group w & 3, row n)
+    // after the last block processed
+    __shared__ __attribute__((aligned(1024))) uint8_t Kst[PAIR ? 2 * K_BYTES : 1];
+    __shared__ __attribute__((aligned(1024))) uint8_t Vst[PAIR ? 2 * V_BYTES : 1];
+    __shared__ float mslot[PAIR ? NW / 2 : 1][32];
 
     // Chunk swizzles: LDS row r of a stage stores logical 16-byte chunk L at
     // physical chunk L ^ swz(r).  kswz spreads the 16 rows read by a 16-lane
@@ -118,15 +164,16 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     // LDS row of a K stage -> key offset in the block
     auto krow_key = [](int r) __attribute__((always_inline)) { return 32 * (r >> 5) + a_row_to_key(r & 31); };
 
-    // ---- persistent loop over this workgroup's tile pairs (heavier tile first) ----
+    // ---- persistent loop over this workgroup's tile pairs (heavier tile first;
+    // PAIR: single tiles, p.pairs = n_tiles) ----
     const UnitRange ur = unit_range(p);
     const int T = p.n_tiles;
     for (long long u = ur.begin + ur.first; u < ur.end; u += ur.stride) {
     for (int half = 0; half < 2; ++half) {
         const int bh = (int)(u / p.pairs);
         const int pr = (int)(u - (long long)bh * p.pairs);
-        const int tile = half == 0 ? T - 1 - pr : pr;
-        if (half == 1 && tile == T - 1 - pr)
+        const int tile = PAIR ? pr : half == 0 ? T - 1 - pr : pr;
+        if (half == 1 && (PAIR || tile == T - 1 - pr))
             break;                                    // odd tile count: the middle tile is alone
         // N query rows; Nk keys; row r at key position r + qoff (qoff = 0 for
         // self-attention; otherwise a multiple of BC, so that every row of a
@@ -142,7 +189,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         const int n = lane & 31;
         const int h = lane >> 5;
         const int row0 = tile * BM;
-        const int wrow0 = row0 + 32 * w;
+        const int wrow0 = row0 + 32 * (PAIR ? (w & 3) : w);
         const int row = wrow0 + n;
 
         const uint8_t* Qg = static_cast<const uint8_t*>(p.q) + (size_t)bh * N * KROW;
@@ -180,32 +227,32 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         }
         const uint32_t k_voff = (uint32_t)k_key_l * KROW + k_chunk_l;
         const uint32_t v_voff = (uint32_t)v_key_l * VROW + v_chunk_l;
-        auto load_k = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+        auto load_k = [&](auto dst, int j) __attribute__((always_inline)) {
             const int t0 = j * BC;
             if (t0 + BC <= Nk) {
 #pragma unroll
                 for (int it = 0; it < K_NI; ++it)
                     g2lds16(Kg + (size_t)(t0 + krow_key(4 * K_RPI * it)) * KROW, k_voff,
-                            dst + (wl + 4 * it) * 1024);
+                            lds_addr(dst) + (wl + 4 * it) * 1024);
             } else {
 #pragma unroll
                 for (int it = 0; it < K_NI; ++it) {
                     const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, Nk - 1);
-                    g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, dst + (wl + 4 * it) * 1024);
+                    g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, lds_addr(dst) + (wl + 4 * it) * 1024);
                 }
             }
         };
-        auto load_v = [&](uint8_t* dst, int j) __attribute__((always_inline)) {
+        auto load_v = [&](auto dst, int j) __attribute__((always_inline)) {
             const int t0 = j * BC;
             if (t0 + BC <= Nk) {
 #pragma unroll
                 for (int it = 0; it < V_NI; ++it)
-                    g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, dst + (wl + 4 * it) * 1024);
+                    g2lds16(Vg + (size_t)(t0 + 4 * V_RPI * it) * VROW, v_voff, lds_addr(dst) + (wl + 4 * it) * 1024);
             } else {
 #pragma unroll
                 for (int it = 0; it < V_NI; ++it) {
                     const int key = min(t0 + 4 * V_RPI * it + v_key_l, Nk - 1);
-                    g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, dst + (wl + 4 * it) * 1024);
+                    g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, lds_addr(dst) + (wl + 4 * it) * 1024);
                 }
             }
         };
@@ -264,7 +311,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         // CU-wide LDS bandwidth (shared with three other waves in this phase)
         // overlap the matrix core; sched_barrier keeps the compiler from sinking
         // the reads back next to their uses.
-        auto qk = [&](const uint8_t* kst) __attribute__((always_inline)) {
+        // (PAIR: kst is the stage's LDS address)
+        auto qk = [&](auto kst) __attribute__((always_inline)) {
             auto kfrag = [&](int kk, int kt) __attribute__((always_inline)) {
                 if constexpr (QK8) {
                     const i32x4 lo = *reinterpret_cast<const i32x4*>(kst + (k_lane ^ (uint32_t)(kk << 6)) + kt * 32 * KROW);
@@ -274,20 +322,39 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                     return *reinterpret_cast<const bf16x8*>(kst + (k_lane ^ (uint32_t)(kk << 5)) + kt * 32 * KROW);
                 }
             };
+            // the KT fragments of k-step kk
+            auto kstep = [&](int kk, QFrag* dst) __attribute__((always_inline)) {
+                if constexpr (PAIR) {
+                    if constexpr (QK8) {
+                        const uint32_t b0 = lds_base(kst + (lds_base(k_lane) ^ (uint32_t)(kk << 6)));
+                        const uint32_t b1 = lds_base(kst + (lds_base(k_lane1) ^ (uint32_t)(kk << 6)));
+#pragma unroll
+                        for (int kt = 0; kt < KT; ++kt) {
+                            const i32x4 lo = lds_load<i32x4>(b0 + kt * 32 * KROW);
+                            const i32x4 hi = lds_load<i32x4>(b1 + kt * 32 * KROW);
+                            dst[kt] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                        }
+                    } else {
+                        const uint32_t b0 = lds_base(kst + (lds_base(k_lane) ^ (uint32_t)(kk << 5)));
+#pragma unroll
+                        for (int kt = 0; kt < KT; ++kt)
+                            dst[kt] = lds_load<bf16x8>(b0 + kt * 32 * KROW);
+                    }
+                } else {
+#pragma unroll
+                    for (int kt = 0; kt < KT; ++kt)
+                        dst[kt] = kfrag(kk, kt);
+                }
+            };
             constexpr int PF = DK >= 3 ? 2 : DK - 1;    // prefetch distance in k-steps
             QFrag a[PF + 1][KT];
 #pragma unroll
             for (int kk = 0; kk < PF; ++kk)
-#pragma unroll
-                for (int kt = 0; kt < KT; ++kt)
-                    a[kk][kt] = kfrag(kk, kt);
+                kstep(kk, a[kk]);
 #pragma unroll
             for (int kk = 0; kk < DK; ++kk) {
-                if (kk + PF < DK) {
-#pragma unroll
-                    for (int kt = 0; kt < KT; ++kt)
-                        a[(kk + PF) % (PF + 1)][kt] = kfrag(kk + PF, kt);
-                }
+                if (kk + PF < DK)
+                    kstep(kk + PF, a[(kk + PF) % (PF + 1)]);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int kt = 0; kt < KT; ++kt) {
@@ -304,15 +371,29 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
 
         // ---- O^T += V_j^T P8^T ----
         // The V^T operands are read (transposed) two MFMAs ahead of their use.
-        auto pv = [&](const uint8_t* vst) __attribute__((always_inline)) {
+        // (PAIR: vst is the stage's LDS address)
+        auto pv = [&](auto vst) __attribute__((always_inline)) {
             auto vload = [&](int i) __attribute__((always_inline)) {
                 const int js = i / DT, dt = i % DT;
-                const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
-                const i32x2 r0 = lds_read_tr8(va);
-                const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
-                const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
-                const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
-                return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+                if constexpr (PAIR) {
+                    const uint32_t va = lds_base(vst + (lds_base(v_lane) ^ (uint32_t)(dt << 5))) + 64 * js * VROW;
+                    auto tr8 = [](uint32_t a) __attribute__((always_inline)) {
+                        return __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+                            reinterpret_cast<__attribute__((address_space(3))) i32x2*>((uintptr_t)a));
+                    };
+                    const i32x2 r0 = tr8(va);
+                    const i32x2 r1 = tr8(va + 8 * VROW);
+                    const i32x2 r2 = tr8(va + 32 * VROW);
+                    const i32x2 r3 = tr8(va + 40 * VROW);
+                    return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+                } else {
+                    const uint8_t* va = vst + (v_lane ^ (uint32_t)(dt << 5)) + 64 * js * VROW;
+                    const i32x2 r0 = lds_read_tr8(va);
+                    const i32x2 r1 = lds_read_tr8(va + 8 * VROW);
+                    const i32x2 r2 = lds_read_tr8(va + 32 * VROW);
+                    const i32x2 r3 = lds_read_tr8(va + 40 * VROW);
+                    return i32x8{r0[0], r0[1], r1[0], r1[1], r2[0], r2[1], r3[0], r3[1]};
+                }
             };
             constexpr int NM = PVS * DT;                 // FP8 MFMAs per block
             constexpr int PF = NM >= 3 ? 2 : NM - 1;
@@ -375,7 +456,14 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             for (int kt = 1; kt < KT; ++kt)
                 mx = fmax_f(mx, mk[kt]);
             mx = halves_max(mx);
-            const float m_new = fmax_f(m_run, mx);
+            // PAIR: the running maximum after the previous block of the visit
+            // (the partner's, or an earlier one if the partner skipped its
+            // blocks) comes from LDS; alpha still takes this wave's own (O, l)
+            // from its last block to the new maximum
+            float m_prev = m_run;
+            if constexpr (PAIR)
+                m_prev = mslot[w & 3][n];
+            const float m_new = fmax_f(m_prev, mx);
             const float mc_new = m_new * c;
             const float alpha = __builtin_amdgcn_exp2f(mc_run - mc_new);
             const float nmc = -mc_new;
@@ -518,11 +606,20 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             ell = alpha * ell + lsum;
             m_run = m_new;
             mc_run = mc_new;
+            if constexpr (PAIR)
+                mslot[w & 3][n] = m_new;
         };
 
         // ---- prologue: K of the first block into stage 0 ----
-        if (grp == 0)
-            load_k(Ks0, jof(0));
+        if constexpr (PAIR) {
+            if (grp == 0) {
+                load_k(Kst, jof(0));
+                mslot[w][n] = -INFINITY;
+            }
+        } else {
+            if (grp == 0)
+                load_k(Ks0, jof(0));
+        }
         // Q fragments and the first K stage are complete after this point; the
         // compiler sees the wait (it tracks no outstanding loads in the loop)
         __builtin_amdgcn_s_waitcnt(0);
@@ -537,44 +634,146 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         // unrolled twice so every LDS access names its stage statically).
         if (grp == 1)
             __syncthreads();
-        auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
-            __attribute__((always_inline)) {
-            if (grp == 0) {
-                if (k + 1 < nb)
-                    load_k(k_nxt, jof(k + 1));
-                if (k < nb)
-                    load_v(v_cur, jof(k));
-            }
-            // the wave in its MFMA phase takes issue priority over its SIMD
-            // partner in the VALU phase, so the matrix core is fed first
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_setprio(1);
-            __builtin_amdgcn_sched_barrier(0);
-            if (valid(k - 1))
-                pv(v_prv);
-            if (valid(k))
-                qk(k_cur);
-            __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_setprio(0);
-            __builtin_amdgcn_sched_barrier(0);
-            __syncthreads();
-            if (valid(k))
-                softmax(jof(k));
-            // the stage loads issued in the MFMA phase must land before the
-            // barrier that hands them to the next MFMA phase
-            if (grp == 0)
+        if constexpr (PAIR) {
+            // PAIR: group g processes the blocks at visit positions k = 2 i + g.
+            // Its MFMA phase i (P.V of its previous block k - 2, S^T of block k)
+            // is phase k of the workgroup and its softmax of block k phase k + 1,
+            // so block k's softmax follows block k - 1's (the partner's) with a
+            // barrier between them.  K_k is read only in phase k and V_k only in
+            // phase k + 2, both from stage k % 2 = g: a group reads its own
+            // stages and, at the start of its MFMA phase k, copies K_{k+1} and
+            // V_{k-1} into the other group's (last read in phase k - 1), waiting
+            // for them at the end of the phase.  (A third stage, copied two
+            // phases ahead from either side of the phase, measured slower.)
+            const uint32_t k_own = lds_addr(Kst) + (uint32_t)(grp * K_BYTES);
+            const uint32_t k_oth = lds_addr(Kst) + (uint32_t)((1 - grp) * K_BYTES);
+            const uint32_t v_own = lds_addr(Vst) + (uint32_t)(grp * V_BYTES);
+            const uint32_t v_oth = lds_addr(Vst) + (uint32_t)((1 - grp) * V_BYTES);
+            auto pair_iteration = [&](int i) __attribute__((always_inline)) {
+                const int kq = 2 * i + grp;
+                if (kq + 1 < nb)
+                    load_k(k_oth, jof(kq + 1));
+                if (kq >= 1 && kq - 1 < nb)
+                    load_v(v_oth, jof(kq - 1));
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(1);
+                __builtin_amdgcn_sched_barrier(0);
+                if (valid(kq - 2))
+                    pv(v_own);
+                if (valid(kq))
+                    qk(k_own);
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(0);
+                __builtin_amdgcn_sched_barrier(0);
                 wait_loads();
-            __syncthreads();
-        };
-        for (int k = 0; k <= nb; k += 2) {
-            iteration(k, Ks0, Ks1, Vs0, Vs1);
-            if (k + 1 <= nb)
-                iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
+                __syncthreads();
+                if (valid(kq))
+                    softmax(jof(kq));
+                __syncthreads();
+            };
+            // both groups pass the same number of barriers; the last P.V of
+            // a group comes two phases after its last block
+            const int I = (nb + 3) / 2;
+            for (int i = 0; i < I; ++i)
+                pair_iteration(i);
+        } else {
+            auto iteration = [&](int k, uint8_t* k_cur, uint8_t* k_nxt, uint8_t* v_cur, uint8_t* v_prv)
+                __attribute__((always_inline)) {
+                if (grp == 0) {
+                    if (k + 1 < nb)
+                        load_k(k_nxt, jof(k + 1));
+                    if (k < nb)
+                        load_v(v_cur, jof(k));
+                }
+                // the wave in its MFMA phase takes issue priority over its SIMD
+                // partner in the VALU phase, so the matrix core is fed first
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(1);
+                __builtin_amdgcn_sched_barrier(0);
+                if (valid(k - 1))
+                    pv(v_prv);
+                if (valid(k))
+                    qk(k_cur);
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_setprio(0);
+                __builtin_amdgcn_sched_barrier(0);
+                __syncthreads();
+                if (valid(k))
+                    softmax(jof(k));
+                // the stage loads issued in the MFMA phase must land before the
+                // barrier that hands them to the next MFMA phase
+                if (grp == 0)
+                    wait_loads();
+                __syncthreads();
+            };
+            for (int k = 0; k <= nb; k += 2) {
+                iteration(k, Ks0, Ks1, Vs0, Vs1);
+                if (k + 1 <= nb)
+                    iteration(k + 1, Ks1, Ks0, Vs1, Vs0);
+            }
         }
         if (grp == 0)
             __syncthreads();
 
-        if (!wave_on)
+        if constexpr (PAIR) {
+            // The row group's two partials.  This wave's (O, l) is at the
+            // maximum of its own last block; bring it to the rows' final
+            // maximum (the slot after the last block of the visit), then
+            // group 1 hands its partial to group 0 through LDS: O through K
+            // stage 1 in rounds of XR 16-byte pieces per lane, l and the
+            // counts through V stage 0.  K stage 0 is left alone (the next
+            // tile's first K block lands there before its first barrier).  (Rows whose
+            // waves saw no block keep -inf: factor 1.)
+            const float mc_f = mslot[w & 3][n] * c;
+            const float a = mc_run == mc_f ? 1.0f : __builtin_amdgcn_exp2f(mc_run - mc_f);
+            ell *= a;
+#pragma unroll
+            for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    o[dt][r] *= a;
+            mc_run = mc_f;
+            constexpr int XR = K_BYTES / 4096 < 4 * DT ? K_BYTES / 4096 : 4 * DT;   // pieces per round
+            static_assert(XR >= 1 && (4 * DT) % XR == 0 && V_BYTES >= 4096, "handoff layout");
+            f32x4* const xw = reinterpret_cast<f32x4*>(Kst + K_BYTES) + ((w & 3) * 64 + lane) * XR;
+            float* const xsw = reinterpret_cast<float*>(Vst) + ((w & 3) * 64 + lane) * 4;
+            if (grp == 1) {
+                xsw[0] = ell;
+                xsw[1] = __uint_as_float(cnt0);
+                xsw[2] = __uint_as_float(cnt1);
+                xsw[3] = __uint_as_float(cnt2);
+            }
+#pragma unroll
+            for (int r0 = 0; r0 < 4 * DT; r0 += XR) {
+                if (grp == 1) {
+#pragma unroll
+                    for (int x = 0; x < XR; ++x) {
+                        const int dt = (r0 + x) / 4, r4 = (r0 + x) % 4;
+                        xw[x] = f32x4{o[dt][4 * r4], o[dt][4 * r4 + 1], o[dt][4 * r4 + 2], o[dt][4 * r4 + 3]};
+                    }
+                }
+                __syncthreads();
+                if (grp == 0) {
+#pragma unroll
+                    for (int x = 0; x < XR; ++x) {
+                        const int dt = (r0 + x) / 4, r4 = (r0 + x) % 4;
+                        const f32x4 x4 = xw[x];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            o[dt][4 * r4 + e] += x4[e];
+                    }
+                    if (r0 == 0) {
+                        ell += xsw[0];
+                        cnt0 += __float_as_uint(xsw[1]);
+                        cnt1 += __float_as_uint(xsw[2]);
+                        cnt2 += __float_as_uint(xsw[3]);
+                    }
+                }
+                __syncthreads();
+            }
+        }
+
+        if (!wave_on || (PAIR && grp == 1))
             continue;
         const float ell_row = ell + other_half(ell);
         if (COUNT) {

@@ -1,0 +1,6 @@
+// bf16 Q/K instantiations of the fast kernel, 128-row (paired) schedule.
+#include "attn_fast_dispatch.hpp"
+
+namespace attn {
+template hipError_t launch_fast_t<false, true>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+}  // namespace attn

@@ -1,0 +1,7 @@
+// E4M3 Q/K instantiations of the fast kernel (S^T on the FP8 MFMA), 128-row
+// (paired) schedule.
+#include "attn_fast_dispatch.hpp"
+
+namespace attn {
+template hipError_t launch_fast_t<true, true>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+}  // namespace attn

@@ -22,7 +22,7 @@ __device__ __align__(256) uint8_t scratch[kScratchBytes];
 
 namespace {
 
-constexpr int kVersion = 610;   // 0.6.1: allocation-free KV-cache entry point
+constexpr int kVersion = 620;   // 0.6.2: 128-row schedule of the fast kernel (ATTN_TILE_*)
 
 // Clears the diagnostic's output arrays on the caller's stream (a kernel, not
 // a memset node, so the call stays safe inside a captured graph).
@@ -44,6 +44,7 @@ bool is_pow2_scale(float S)
 struct Call {
     attn::Params p;
     int d, block_kv, mode;
+    int tile;   // fast kernel rows per tile asked for: 256, 128 or 0 (chosen at launch)
     bool causal, count, dyn, fast, prefill, empty;
 };
 
@@ -53,8 +54,11 @@ int prepare(Call& cl, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, 
             int block_kv, int order, float S, int mode_flags, int n_sink, float q_descale,
             float k_descale, float v_descale)
 {
-    const int mode = mode_flags & ~ATTN_SCALE_DYNAMIC;
+    const int mode = mode_flags & ~(ATTN_SCALE_DYNAMIC | ATTN_TILE_256 | ATTN_TILE_128);
     const bool dyn = (mode_flags & ATTN_SCALE_DYNAMIC) != 0;
+    if ((mode_flags & ATTN_TILE_256) && (mode_flags & ATTN_TILE_128))
+        return ATTN_ERR_INVALID_ARG;
+    cl.tile = (mode_flags & ATTN_TILE_256) ? 256 : (mode_flags & ATTN_TILE_128) ? 128 : 0;
     if (B < 0 || Hq < 1 || Hkv < 1 || N < 0 || Nk < N || Hq % Hkv != 0)
         return ATTN_ERR_INVALID_ARG;
     if (causal != 0 && causal != 1)
@@ -103,8 +107,10 @@ int prepare(Call& cl, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, 
     // short ones, or unaligned offsets, on the prefill kernel, whose waves
     // share a 32-row tile's KV blocks.
     cl.prefill = cl.fast && Nk != N && (N < 128 || (Nk - N) % block_kv != 0);
+    // (the fast kernel's tiles are counted at 256 rows here; a launch that
+    // picks the 128-row schedule recounts them)
     const int bm = cl.prefill ? attn::prefill_rows_per_wg()
-                              : cl.fast ? attn::fast_rows_per_wg(d, block_kv) : attn::faithful_rows_per_wg();
+                              : cl.fast ? attn::kFastRows : attn::faithful_rows_per_wg();
     const int64_t n_tiles = ((int64_t)N + bm - 1) / bm;
     const int64_t total = (int64_t)B * Hq * n_tiles;
     // element offsets stay within 64-bit; the grid must fit a 1-D launch
@@ -207,15 +213,29 @@ int launch(Call& cl, const void* q, const void* k, const void* v, float* out, fl
         e = attn::launch_prefill(p, cl.d, cl.block_kv, cl.causal, cl.count, scale,
                                  cl.mode == ATTN_MODE_FP8QK, n_cu, ws, ws_bytes, s);
     } else if (cl.fast) {
+        // Schedule: 256-row tiles in causal-balanced pairs, unless that
+        // leaves at least half of the CUs without a unit (or the caller asked):
+        // then 128-row tiles, one per unit, two waves per 32-row group.
+        const bool pair = cl.tile == 128 || (cl.tile == 0 && p.units * 2 <= n_cu);
+        if (pair) {
+            const long long n_tiles = ((long long)p.N + attn::kFastRowsPair - 1) / attn::kFastRowsPair;
+            const long long total = (long long)p.B * p.Hq * n_tiles;
+            p.n_tiles = (int)n_tiles;
+            p.total_wg = (int)total;
+            p.per_xcd = (int)((total + attn::kNumXcd - 1) / attn::kNumXcd);
+            p.pairs = (int)n_tiles;
+            p.units = total;
+        }
         // persistent grid: one workgroup per CU (the LDS footprint admits no
         // second one), 8 XCDs, never more workgroups than work units
         const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
         const long long per_xcd = p.units / attn::kNumXcd + 1 < per_xcd_max ? p.units / attn::kNumXcd + 1
                                                                             : per_xcd_max;
         const int grid = (int)(per_xcd * attn::kNumXcd);
-        e = cl.mode == ATTN_MODE_FP8QK
-                ? attn::launch_fast_qk8(p, grid, cl.d, cl.block_kv, cl.causal, cl.count, scale, s)
-                : attn::launch_fast(p, grid, cl.d, cl.block_kv, cl.causal, cl.count, scale, s);
+        const bool qk8 = cl.mode == ATTN_MODE_FP8QK;
+        auto go = [&](auto fn) { return fn(p, grid, cl.d, cl.block_kv, cl.causal, cl.count, scale, s); };
+        e = qk8 ? (pair ? go(attn::launch_fast_t<true, true>) : go(attn::launch_fast_t<true, false>))
+                : (pair ? go(attn::launch_fast_t<false, true>) : go(attn::launch_fast_t<false, false>));
     } else {
         e = attn::launch_faithful(p, cl.d, cl.block_kv, cl.causal, cl.count,
                                   cl.mode == ATTN_MODE_FAITHFUL, cl.dyn, s);

@@ -10,13 +10,21 @@ hipError_t launch_faithful(const Params& p, int d, int block_kv, bool causal, bo
                            bool cast, bool dynamic, hipStream_t stream);
 int faithful_rows_per_wg();
 
-// grid: a multiple of 8 workgroups, at most one per CU (persistent kernel)
-hipError_t launch_fast(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
-                       int scale /* kScale* */, hipStream_t stream);
-// the same kernel with E4M3 Q and K (S^T on the FP8 MFMA)
-hipError_t launch_fast_qk8(const Params& p, int grid, int d, int block_kv, bool causal, bool count,
-                           int scale /* kScale* */, hipStream_t stream);
-int fast_rows_per_wg(int d, int block_kv);
+// The fast kernel (persistent): QK8 selects E4M3 Q and K (S^T on the FP8
+// MFMA), PAIR the 128-row schedule (two waves per 32-row group, alternate
+// blocks).  grid: a multiple of 8 workgroups, at most one per CU; scale: kScale*.
+// Each (QK8, PAIR) pair is instantiated in its own translation unit.
+template <bool QK8, bool PAIR>
+hipError_t launch_fast_t(const Params& p, int grid, int d, int block_kv, bool causal, bool count, int scale,
+                         hipStream_t stream);
+extern template hipError_t launch_fast_t<false, false>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+extern template hipError_t launch_fast_t<false, true>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+extern template hipError_t launch_fast_t<true, false>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+extern template hipError_t launch_fast_t<true, true>(const Params&, int, int, int, bool, bool, int, hipStream_t);
+// query rows per tile (one work unit of the 128-row schedule, half of one
+// of the 256-row schedule's tile pairs)
+constexpr int kFastRows = 256;
+constexpr int kFastRowsPair = 128;
 
 // queries against a longer KV cache (p.Nk > p.N), fast modes: one workgroup
 // per (batch, head, 32-row query tile), or several per tile when the tiles

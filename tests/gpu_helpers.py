@@ -41,15 +41,16 @@ def to_device(inp):
 
 
 def run_gpu(dev, mode, S, order, causal, block_kv, n_sink=4, counts=True, scale="static",
-            descales=(1.0, 1.0, 1.0)):
+            descales=(1.0, 1.0, 1.0), tile=None):
     from paper_2606_06521_amd import attn_fp8 as A
     q, k, v = dev
     out, lse = A.fwd(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv, mode=mode,
-                     scale=scale, descales=descales)
+                     scale=scale, descales=descales, tile=tile)
     cnt = None
     if counts:
         cnt = A.p_underflow_count(q, k, v, S=S, order=order, causal=causal, block_kv=block_kv,
-                                  mode=mode, n_sink=n_sink, scale=scale, descales=descales)
+                                  mode=mode, n_sink=n_sink, scale=scale, descales=descales,
+                                  tile=tile)
     torch.cuda.synchronize()
     res = (out.cpu().numpy(), lse.cpu().numpy(), None if cnt is None else cnt.cpu().numpy().view(np.uint32))
     return res

@@ -8,7 +8,11 @@
 //   - the per-lane E8M0 operand scales of the block-scaled FP8 MFMA and the
 //     per-lane scale of the scaled convert (the dynamic P-scale),
 //   - the chip-wide issue rate of v_exp_f32 (the exp2 peak the attention
-//     kernels are measured against).
+//     kernels are measured against),
+//   - the LDS read rate of one CU (ds_read_b128 and the transposing
+//     ds_read_b64_tr_b8, the two reads of the MFMA phase), alone and while
+//     other waves of the workgroup copy global memory into LDS with
+//     global_load_lds_dwordx4 (the stage copies).
 // Every kernel bounds-checks its index against n.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -17,6 +21,8 @@ typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 typedef __attribute__((__vector_size__(8 * sizeof(int)))) int i32x8;
 typedef __attribute__((__vector_size__(2 * sizeof(short)))) short s16x2;
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(int)))) int i32x2;
 
 __global__ void k_cvt_range(uint32_t lo, int64_t n, uint8_t* out)
 {
@@ -81,6 +87,79 @@ __global__ void __launch_bounds__(256) k_exp2_rate(int iters, float* out)
     for (int i = 0; i < 16; ++i)
         acc += x[i];
     out[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
+// LDS read rate.  One workgroup of 8 waves per CU.  Reader waves issue
+// rounds of 8 independent reads (mode bit 0: 0 = ds_read_b128, 1 KB per wave
+// instruction; 1 = ds_read_b64_tr_b8, 512 B) over their own 8 KB of LDS, then
+// wait for them; cycles[wg * 8 + wave] gets the s_memtime cycles of the read
+// loop.  readers: waves 0..readers-1 read.  copiers: waves 8-copiers..7 copy
+// 1 KB per instruction from src (64 KB, L2-resident after the first round)
+// into a separate 16 KB of LDS with global_load_lds_dwordx4, keeping at most
+// 8 copies in flight, for as many rounds as the readers run (iters * 8
+// instructions); a wave is never both.  sink keeps the reads alive.
+__global__ void __launch_bounds__(512) k_lds_rate(int iters, int mode, int readers, int copiers,
+                                                   const uint8_t* src, unsigned long long* cycles,
+                                                   uint32_t* sink)
+{
+    __shared__ __attribute__((aligned(1024))) uint32_t buf[16384];    // 64 KB: 8 KB per reader wave
+    __shared__ __attribute__((aligned(1024))) uint8_t cbuf[32768];    // copy target (16 KB used; 96 KB in all: one workgroup per CU)
+    for (int i = threadIdx.x; i < 16384; i += 512)
+        buf[i] = (uint32_t)i * 2654435761u;
+    __syncthreads();
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    uint32_t acc = 0;
+    unsigned long long t0 = 0, t1 = 0;
+    if (w < readers) {
+        const uint32_t a = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint32_t*)(buf + w * 2048) +
+                           (mode ? 8u : 16u) * (uint32_t)lane;
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+        for (int it = 0; it < iters; ++it) {
+            if (mode == 0) {
+                i32x4 r0, r1, r2, r3, r4, r5, r6, r7;
+                asm volatile(
+                    "ds_read_b128 %0, %8\n\tds_read_b128 %1, %8 offset:1024\n\t"
+                    "ds_read_b128 %2, %8 offset:2048\n\tds_read_b128 %3, %8 offset:3072\n\t"
+                    "ds_read_b128 %4, %8 offset:4096\n\tds_read_b128 %5, %8 offset:5120\n\t"
+                    "ds_read_b128 %6, %8 offset:6144\n\tds_read_b128 %7, %8 offset:7168\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=v"(r0), "=v"(r1), "=v"(r2), "=v"(r3), "=v"(r4), "=v"(r5), "=v"(r6), "=v"(r7)
+                    : "v"(a) : "memory");
+                acc ^= (uint32_t)(r0[0] ^ r1[1] ^ r2[2] ^ r3[3] ^ r4[0] ^ r5[1] ^ r6[2] ^ r7[3]);
+            } else {
+                i32x2 r0, r1, r2, r3, r4, r5, r6, r7;
+                asm volatile(
+                    "ds_read_b64_tr_b8 %0, %8\n\tds_read_b64_tr_b8 %1, %8 offset:512\n\t"
+                    "ds_read_b64_tr_b8 %2, %8 offset:1024\n\tds_read_b64_tr_b8 %3, %8 offset:1536\n\t"
+                    "ds_read_b64_tr_b8 %4, %8 offset:2048\n\tds_read_b64_tr_b8 %5, %8 offset:2560\n\t"
+                    "ds_read_b64_tr_b8 %6, %8 offset:3072\n\tds_read_b64_tr_b8 %7, %8 offset:3584\n\t"
+                    "s_waitcnt lgkmcnt(0)"
+                    : "=v"(r0), "=v"(r1), "=v"(r2), "=v"(r3), "=v"(r4), "=v"(r5), "=v"(r6), "=v"(r7)
+                    : "v"(a) : "memory");
+                acc ^= (uint32_t)(r0[0] ^ r1[1] ^ r2[0] ^ r3[1] ^ r4[0] ^ r5[1] ^ r6[0] ^ r7[1]);
+            }
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
+    } else if (w >= 8 - copiers) {
+        // copy instruction i: 1 KB from src + 1024 * (i % 64), lane l -> +16 l;
+        // LDS cbuf + 1024 * (i % 16)
+        const uint32_t lds0 = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) uint8_t*)cbuf;
+        const uint32_t voff = 16u * (uint32_t)lane;
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+        for (int i = 0; i < iters * 8; ++i) {
+            const uint8_t* base = src + 1024 * (i & 63);
+            const uint32_t m0 = lds0 + 1024u * (uint32_t)(i & 15);
+            asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2\n\ts_waitcnt vmcnt(8)"
+                         :
+                         : "s"(__builtin_amdgcn_readfirstlane(m0)), "v"(voff), "s"(base)
+                         : "memory");
+        }
+        asm volatile("s_waitcnt vmcnt(0)\n\ts_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
+    }
+    if (lane == 0)
+        cycles[blockIdx.x * 8 + w] = t1 - t0;
+    sink[blockIdx.x * 512 + threadIdx.x] = acc;
 }
 
 // One wave.  A: 32x16 bf16 (row-major), B: 16x32 bf16, D: 32x32 f32.
@@ -241,6 +320,17 @@ int probe_exp2_rate(int blocks, int iters, float* out, void* stream)
     if (blocks <= 0 || iters <= 0 || !out)
         return -1;
     hipLaunchKernelGGL(k_exp2_rate, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters, out);
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+int probe_lds_rate(int blocks, int iters, int mode, int readers, int copiers, const void* src,
+                   unsigned long long* cycles, uint32_t* sink, void* stream)
+{
+    if (blocks <= 0 || iters <= 0 || mode < 0 || mode > 1 || readers < 0 || copiers < 0 ||
+        readers + copiers > 8 || !cycles || !sink || (copiers > 0 && !src))
+        return -1;
+    hipLaunchKernelGGL(k_lds_rate, dim3(blocks), dim3(512), 0, (hipStream_t)stream, iters, mode, readers,
+                       copiers, (const uint8_t*)src, cycles, sink);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

@@ -50,8 +50,9 @@ def test_enum_values_match_header(A):
                  "ATTN_ERR_HIP", "ATTN_ERR_SCRATCH"]:
         m = re.search(name + r"\s*=\s*(-?\d+)", text)
         assert m and int(m.group(1)) == getattr(A, name), name
-    m = re.search(r"ATTN_SCALE_DYNAMIC\s*=\s*(0x[0-9a-fA-F]+)", text)
-    assert m and int(m.group(1), 16) == A.ATTN_SCALE_DYNAMIC
+    for name in ["ATTN_SCALE_DYNAMIC", "ATTN_TILE_256", "ATTN_TILE_128"]:
+        m = re.search(name + r"\s*=\s*(0x[0-9a-fA-F]+)", text)
+        assert m and int(m.group(1), 16) == getattr(A, name), name
 
 
 FAKE = 0x1000   # never dereferenced: every case below fails validation first
@@ -73,9 +74,11 @@ def fwd(A, **kw):
     (dict(S=0.0), -1), (dict(S=-1.0), -1), (dict(S=float("inf")), -1), (dict(S=float("nan")), -1),
     (dict(d=96), -2), (dict(d=256), -2), (dict(block_kv=32), -2), (dict(block_kv=256), -2),
     (dict(d=0), -1),
-    # the dynamic scale needs S = 2^k0 with 0 <= k0 <= 8, and no other flag bit exists
+    # the dynamic scale needs S = 2^k0 with 0 <= k0 <= 8; at most one ATTN_TILE_* flag;
+    # no other flag bit exists
     (dict(mode=1 | 0x100, S=3.0), -1), (dict(mode=1 | 0x100, S=512.0), -1),
-    (dict(mode=0 | 0x100, S=0.5), -1), (dict(mode=1 | 0x200), -1), (dict(mode=1 | 0x80), -1),
+    (dict(mode=0 | 0x100, S=0.5), -1), (dict(mode=1 | 0x600), -1), (dict(mode=1 | 0x800), -1),
+    (dict(mode=1 | 0x80), -1),
 ])
 def test_fwd_rejects_bad_arguments(A, kw, status):
     assert fwd(A, **kw) == status

@@ -18,27 +18,28 @@ pytestmark = pytest.mark.gpu
 FMT = {"faithful": "f32", "fast": "bf16_e4m3", "fp8qk": "e4m3"}
 
 
-def _run(dev, mode, S, order, causal, bkv, scale="static", nbins=32):
+def _run(dev, mode, S, order, causal, bkv, scale="static", nbins=32, tile=None):
     from paper_2606_06521_amd import attn_fp8 as A
     q, k, v = dev
     hist, bz, cnt = A.block_gap_diag(q, k, v, S=S, order=order, causal=causal, block_kv=bkv,
-                                     mode=mode, nbins=nbins, scale=scale)
+                                     mode=mode, nbins=nbins, scale=scale, tile=tile)
     torch.cuda.synchronize()
     return (hist.cpu().numpy().view(np.uint32), bz.cpu().numpy().view(np.uint32),
             cnt.cpu().numpy().view(np.uint32))
 
 
-@pytest.mark.parametrize("mode", ["faithful", "fast", "fp8qk"])
+@pytest.mark.parametrize("mode,tile", [("faithful", None), ("fast", 256), ("fast", 128),
+                                       ("fp8qk", 256), ("fp8qk", 128)])
 @pytest.mark.parametrize("d,bkv", [(64, 64), (128, 128), (128, 64)])
-def test_small_exact(mode, d, bkv):
+def test_small_exact(mode, tile, d, bkv):
     inp = make_inputs(2, 4, 2, 333, d, fmt=FMT[mode], delta=9.0, seed=800 + d + bkv)
     dev = to_device(inp)
     for (causal, order), (S, scale) in itertools.product(
             itertools.product([False, True], ["forward", "reverse"]),
             [(256.0, "static"), (16.0, "dynamic"), (1.0, "static")]):
-        label = f"diag {mode} d={d} bkv={bkv} causal={causal} {order} S={S} {scale}"
+        label = f"diag {mode} d={d} bkv={bkv} causal={causal} {order} S={S} {scale} tile={tile}"
         log(label)
-        hist, bz, cnt = _run(dev, mode, S, order, causal, bkv, scale)
+        hist, bz, cnt = _run(dev, mode, S, order, causal, bkv, scale, tile=tile)
         _, _, o_cnt, o_hist, o_bz = oracle.block_diag(inp.q32, inp.k32, inp.v32, S=S,
                                                       order=order, block_kv=bkv, causal=causal,
                                                       scale=scale, nbins=32)

@@ -33,11 +33,13 @@ def test_small(mode, d, bkv):
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
+@pytest.mark.parametrize("tile", [256, 128])
 @pytest.mark.parametrize("mode", ["fast", "fp8qk"])
 @pytest.mark.parametrize("bkv", [64, 128])
-def test_long_chunks(mode, bkv):
+def test_long_chunks(mode, bkv, tile):
     # 256 queries with a block-aligned offset (Nk = 640) take the persistent
-    # kernel; 200 queries at offset 133 (Nk = 333) the prefill kernel
+    # kernel (on either schedule); 200 queries at offset 133 (Nk = 333) the
+    # prefill kernel (where the schedule flag has no effect)
     for nk, nq in ((640, 256), (333, 200)):
         full = make_inputs(1, 4, 2, nk, 128, fmt=FMT[mode], delta=9.0, seed=960 + nk + bkv)
         inp = last_queries(full, nq)
@@ -45,9 +47,9 @@ def test_long_chunks(mode, bkv):
         for (causal, order), (S, scale) in itertools.product(
                 itertools.product([False, True], ["forward", "reverse"]),
                 [(256.0, "static"), (448.0, "static"), (16.0, "dynamic")]):
-            label = f"kv {mode} nq={nq} nk={nk} bkv={bkv} causal={causal} {order} S={S} {scale}"
+            label = f"kv {mode} nq={nq} nk={nk} bkv={bkv} causal={causal} {order} S={S} {scale} tile={tile}"
             log(label)
-            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale=scale)
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale=scale, tile=tile)
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale=scale)
 
 
@@ -266,3 +268,36 @@ def test_split_workspace_two_host_threads():
         label = f"kv split two threads, problem {i}"
         log(label)
         compare(probs[i], results[i], "fast", 256.0, "reverse", True, 128, label=label)
+
+
+def test_workload_prefill_q256_full_size_both_schedules():
+    """The KV-cache prefill workload at full size (4 x 32 query heads, 8 KV
+    heads, the last 256 of 32768 positions, d = 128): 128 tiles of 256 rows
+    would leave half of the CUs idle, so the library picks the 128-row
+    schedule.  Both schedules are run.  Their E4M3 codes are the same by
+    construction, so the counts must agree on every row; the outputs only in
+    FP32 rounding.  Sampled rows are checked against the oracle."""
+    w = WORKLOADS["prefill_q256_b4_h32kv8_n32768_d128_fast"]
+    full = make_inputs(w.B, w.Hq, w.Hkv, w.N, w.d, fmt=w.fmt, delta=w.deltas[0], seed=w.seed_base)
+    inp = last_queries(full, w.nq)
+    del full
+    dev = to_device(inp)
+    nq = w.nq
+    rng = np.random.default_rng(5)
+    heads = np.array([0, 45, 127])                      # flat (batch, head) ids
+    rows = np.concatenate([bh * nq + np.concatenate([np.arange(0, 8), rng.integers(0, nq, 16),
+                                                     np.arange(nq - 8, nq)]) for bh in heads])
+    rows = np.unique(rows)
+    res = {}
+    for tile in (None, 128, 256):
+        label = f"{w.name} S=256 reverse tile={tile} (rows {rows.size})"
+        log(label)
+        gpu = run_gpu(dev, w.mode, 256.0, "reverse", w.causal, w.block_kv, tile=tile)
+        log(str(compare(inp, gpu, w.mode, 256.0, "reverse", w.causal, w.block_kv, rows=rows,
+                        label=label)))
+        res[tile] = gpu
+    for tile in (None, 256):
+        assert np.array_equal(res[tile][2], res[128][2]), tile             # counts, every row
+        assert np.allclose(res[tile][0], res[128][0], rtol=1e-5, atol=1e-6), tile
+        assert np.allclose(res[tile][1], res[128][1], rtol=0, atol=1e-5), tile
+    assert np.array_equal(res[None][0], res[128][0])                       # the automatic choice

@@ -33,19 +33,26 @@ def test_small_faithful_and_nocast(d, bkv, causal, order):
         compare(inp, gpu, mode, S, order, causal, bkv, label=label)
 
 
+# both schedules of the fast kernel: 256-row tiles, and 128-row tiles whose
+# two waves per row group take alternate blocks
+TILES = [256, 128]
+
+
+@pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("d,bkv,causal,order", SMALL)
-def test_small_fast(d, bkv, causal, order):
+def test_small_fast(d, bkv, causal, order, tile):
     inp = make_inputs(2, 4, 2, 333, d, fmt="bf16_e4m3", delta=8.0, seed=200 + d + bkv)
     dev = to_device(inp)
     for S in (1.0, 256.0, 448.0, 3.0, 512.0, 0.0625, 1024.0):
-        label = f"fast d={d} bkv={bkv} causal={causal} {order} S={S}"
+        label = f"fast d={d} bkv={bkv} causal={causal} {order} S={S} tile={tile}"
         log(label)
-        gpu = run_gpu(dev, "fast", S, order, causal, bkv)
+        gpu = run_gpu(dev, "fast", S, order, causal, bkv, tile=tile)
         compare(inp, gpu, "fast", S, order, causal, bkv, label=label)
 
 
+@pytest.mark.parametrize("tile", TILES)
 @pytest.mark.parametrize("d,bkv,causal,order", SMALL)
-def test_small_fp8qk(d, bkv, causal, order):
+def test_small_fp8qk(d, bkv, causal, order, tile):
     # E4M3 Q/K/V (scores on the FP8 MFMA), static and dynamic scales, with and
     # without per-tensor descales
     inp = make_inputs(2, 4, 2, 333, d, fmt="e4m3", delta=8.0, seed=600 + d + bkv)
@@ -54,22 +61,24 @@ def test_small_fp8qk(d, bkv, causal, order):
                          (448.0, "static", (1.0, 1.0, 1.0)), (3.0, "static", (1.0, 1.0, 1.0)),
                          (256.0, "static", (0.75, 1.5, 2.0)), (256.0, "dynamic", (1.0, 1.0, 1.0)),
                          (16.0, "dynamic", (1.25, 0.5, 0.5))]:
-        label = f"fp8qk d={d} bkv={bkv} causal={causal} {order} S={S} {scale} descales={ds}"
+        label = f"fp8qk d={d} bkv={bkv} causal={causal} {order} S={S} {scale} descales={ds} tile={tile}"
         log(label)
-        gpu = run_gpu(dev, "fp8qk", S, order, causal, bkv, scale=scale, descales=ds)
+        gpu = run_gpu(dev, "fp8qk", S, order, causal, bkv, scale=scale, descales=ds, tile=tile)
         compare(inp, gpu, "fp8qk", S, order, causal, bkv, label=label, scale=scale, descales=ds)
 
 
 @pytest.mark.parametrize("d,bkv,causal,order", SMALL)
 def test_small_dynamic_scale(d, bkv, causal, order):
-    # dynamic per-block 2^kj scale in both modes: counts exact, outputs to the mode's bar
-    for mode, fmt in (("faithful", "f32"), ("fast", "bf16_e4m3")):
+    # dynamic per-block 2^kj scale in both modes (the fast mode on both
+    # schedules): counts exact, outputs to the mode's bar
+    for mode, fmt, tile in (("faithful", "f32", None), ("fast", "bf16_e4m3", 256),
+                            ("fast", "bf16_e4m3", 128)):
         inp = make_inputs(2, 4, 2, 333, d, fmt=fmt, delta=10.0, seed=500 + d + bkv)
         dev = to_device(inp)
         for S in (1.0, 16.0, 256.0):
-            label = f"dynamic {mode} d={d} bkv={bkv} causal={causal} {order} S={S}"
+            label = f"dynamic {mode} d={d} bkv={bkv} causal={causal} {order} S={S} tile={tile}"
             log(label)
-            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale="dynamic")
+            gpu = run_gpu(dev, mode, S, order, causal, bkv, scale="dynamic", tile=tile)
             compare(inp, gpu, mode, S, order, causal, bkv, label=label, scale="dynamic")
 
 
@@ -109,10 +118,11 @@ def test_edge_lengths(N, mode):
     fmt = {"faithful": "f32", "fast": "bf16_e4m3", "fp8qk": "e4m3"}[mode]
     inp = make_inputs(1, 2, 1, N, 128, fmt=fmt, delta=9.0, seed=300 + N)
     dev = to_device(inp)
-    for causal, order in itertools.product([False, True], ["forward", "reverse"]):
-        label = f"{mode} N={N} causal={causal} {order}"
+    tiles = [None] if mode == "faithful" else TILES
+    for causal, order, tile in itertools.product([False, True], ["forward", "reverse"], tiles):
+        label = f"{mode} N={N} causal={causal} {order} tile={tile}"
         log(label)
-        gpu = run_gpu(dev, mode, 256.0, order, causal, 64)
+        gpu = run_gpu(dev, mode, 256.0, order, causal, 64, tile=tile)
         compare(inp, gpu, mode, 256.0, order, causal, 64, label=label)
 
 

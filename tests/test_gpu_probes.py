@@ -141,6 +141,44 @@ def test_exp2_issue_rate(probes):
     assert 256 * 256 * 2.4e9 / 64 < rate < 256 * 256 * 2.4e9
 
 
+def test_lds_read_rate(probes):
+    """LDS read rate of one CU, in bytes per shader cycle (s_memtime), for the
+    two reads of the fast kernel's MFMA phase: ds_read_b128 (the K operand)
+    and ds_read_b64_tr_b8 (the transposed V operand).  8 reader waves, then 4
+    reader waves alone and beside 4 waves that copy global memory into LDS
+    with global_load_lds_dwordx4 (the stage copies).  One workgroup per CU,
+    256 workgroups; the median over workgroups of (bytes read / the slowest
+    reader's cycles).  The ds_read_b128 checksums are compared with the host."""
+    blocks, iters = 256, 2049
+    cyc = torch.zeros(blocks * 8, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(blocks * 512, dtype=torch.int32, device="cuda")
+    src = torch.zeros(65536, dtype=torch.uint8, device="cuda")
+    s = torch.cuda.current_stream()
+    words = (np.arange(16384, dtype=np.uint64) * 2654435761) % (1 << 32)
+    res = {}
+    for mode, readers, copiers in [(0, 8, 0), (1, 8, 0), (0, 4, 0), (0, 4, 4), (1, 4, 0), (1, 4, 4)]:
+        assert probes.probe_lds_rate(blocks, 64, mode, readers, copiers, src.data_ptr(), cyc.data_ptr(),
+                                     sink.data_ptr(), s.cuda_stream) == 0   # warm-up
+        assert probes.probe_lds_rate(blocks, iters, mode, readers, copiers, src.data_ptr(), cyc.data_ptr(),
+                                     sink.data_ptr(), s.cuda_stream) == 0
+        torch.cuda.synchronize()
+        c = cyc.cpu().numpy().reshape(blocks, 8)[:, :readers].max(axis=1).astype(np.float64)
+        per_instr = 1024 if mode == 0 else 512
+        rate = float(np.median(readers * iters * 8 * per_instr / c))
+        res[(mode, readers, copiers)] = rate
+        print(f"LDS {'ds_read_b128' if mode == 0 else 'ds_read_b64_tr_b8'}: {readers} reader waves, "
+              f"{copiers} copier waves: {rate:.1f} B/cycle per CU", flush=True)
+        assert 16.0 < rate < 1024.0
+        if mode == 0:
+            # an odd number of rounds leaves one round's XOR in every lane
+            got = sink.cpu().numpy().view(np.uint32).reshape(blocks, 8, 64)
+            for w in range(readers):
+                lanes = np.arange(64)
+                idx = [(w * 8192 + 16 * lanes + 1024 * k) // 4 + (k % 4) for k in range(8)]
+                want = np.bitwise_xor.reduce(np.stack([words[i] for i in idx]), axis=0).astype(np.uint32)
+                assert np.all(got[:, w, :] == want[None, :]), w
+
+
 def test_mfma_bf16_layout(probes):
     rng = np.random.default_rng(8)
     A = rng.integers(-8, 9, (32, 16)).astype(np.float32)
