@@ -109,8 +109,9 @@ enum { ATTN_SCALE_DYNAMIC = 0x100 };
  *                  waves of a 32-row group take alternate KV blocks of the
  *                  visit and hand the running maximum to each other, so every
  *                  block still sees the running maximum of Algorithm 1.
- * Neither: ATTN_TILE_256 unless its units would leave at least half of the
- * GPU's compute units idle.  Both: ATTN_ERR_INVALID_ARG.  The two schedules
+ * Neither: ATTN_TILE_256, unless its units leave compute units idle and a
+ * cost model of the two schedules' critical paths favours ATTN_TILE_128.
+ * Both: ATTN_ERR_INVALID_ARG.  The two schedules
  * give identical E4M3 codes and counts; O and l differ only in FP32 rounding
  * (each 128-row group adds two partial sums at the end).  No effect in the
  * other modes or on short query chunks.

@@ -9,6 +9,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <algorithm>
 #include <mutex>
 
 // Scratch of the allocation-free KV-cache entry point (attn_fp8_fwd_kv_noalloc):
@@ -181,6 +182,49 @@ int check_pointers(const Call& cl, const void* q, const void* k, const void* v, 
     return ATTN_OK;
 }
 
+// Critical path of the fast kernel's persistent grid on one schedule, in
+// ping-pong phases: the largest sum of unit costs any workgroup takes, with
+// the kernel's assignment (XCD x owns units [units x / 8, units (x + 1) / 8),
+// its workgroups take every per-th of them).  A tile of the 256-row schedule
+// costs two phases per visited block (plus one block's worth for the last
+// P.V); one of the 128-row schedule one phase per block (plus two), times
+// kPairPhase, the measured length of its phases against the 256-row
+// schedule's (every phase of the 128-row schedule carries a K/V copy burst).
+constexpr double kPairPhase = 1.15;
+
+double fast_critical_path(const attn::Params& p, bool pair, int block_kv, bool causal, int n_cu)
+{
+    const int rows = pair ? attn::kFastRowsPair : attn::kFastRows;
+    const long long T = ((long long)p.N + rows - 1) / rows;
+    const long long per_head = pair ? T : (T + 1) / 2;
+    const long long units = (long long)p.B * p.Hq * per_head;
+    auto tile_cost = [&](long long t) {
+        const long long last = std::min((t + 1) * rows, (long long)p.N) - 1;
+        const long long nb = causal ? (last + p.qoff) / block_kv + 1 : ((long long)p.Nk + block_kv - 1) / block_kv;
+        return pair ? (double)(nb + 2) * kPairPhase : 2.0 * (double)(nb + 1);
+    };
+    auto unit_cost = [&](long long u) {
+        const long long pr = u % per_head;
+        if (pair)
+            return tile_cost(pr);
+        const long long a = T - 1 - pr;
+        return a == pr ? tile_cost(pr) : tile_cost(a) + tile_cost(pr);
+    };
+    const long long per_xcd_max = n_cu >= attn::kNumXcd ? n_cu / attn::kNumXcd : 1;
+    const long long per = std::min(units / attn::kNumXcd + 1, per_xcd_max);
+    double worst = 0.0;
+    for (int x = 0; x < attn::kNumXcd; ++x) {
+        const long long b = units * x / attn::kNumXcd, e = units * (x + 1) / attn::kNumXcd;
+        for (long long slot = 0; slot < per; ++slot) {
+            double sum = 0.0;
+            for (long long u = b + slot; u < e; u += per)
+                sum += unit_cost(u);
+            worst = std::max(worst, sum);
+        }
+    }
+    return worst;
+}
+
 // Enqueues a prepared, validated, non-empty call on stream s.
 int launch(Call& cl, const void* q, const void* k, const void* v, float* out, float* lse,
            uint32_t* counts, uint32_t* gap_hist, uint32_t* blk_zero, int nbins, void* ws,
@@ -213,10 +257,14 @@ int launch(Call& cl, const void* q, const void* k, const void* v, float* out, fl
         e = attn::launch_prefill(p, cl.d, cl.block_kv, cl.causal, cl.count, scale,
                                  cl.mode == ATTN_MODE_FP8QK, n_cu, ws, ws_bytes, s);
     } else if (cl.fast) {
-        // Schedule: 256-row tiles in causal-balanced pairs, unless that
-        // leaves at least half of the CUs without a unit (or the caller asked):
-        // then 128-row tiles, one per unit, two waves per 32-row group.
-        const bool pair = cl.tile == 128 || (cl.tile == 0 && p.units * 2 <= n_cu);
+        // Schedule: 256-row tiles in causal-balanced pairs, unless the caller
+        // asked otherwise or their units leave CUs idle and the 128-row
+        // schedule (one tile per unit, two waves per 32-row group) has the
+        // shorter critical path.
+        bool pair = cl.tile == 128;
+        if (cl.tile == 0 && p.units < n_cu)
+            pair = fast_critical_path(p, true, cl.block_kv, cl.causal, n_cu) <
+                   fast_critical_path(p, false, cl.block_kv, cl.causal, n_cu);
         if (pair) {
             const long long n_tiles = ((long long)p.N + attn::kFastRowsPair - 1) / attn::kFastRowsPair;
             const long long total = (long long)p.B * p.Hq * n_tiles;
