@@ -12,7 +12,11 @@
 //   - the LDS read rate of one CU (ds_read_b128 and the transposing
 //     ds_read_b64_tr_b8, the two reads of the MFMA phase), alone and while
 //     other waves of the workgroup copy global memory into LDS with
-//     global_load_lds_dwordx4 (the stage copies).
+//     global_load_lds_dwordx4 (the stage copies),
+//   - how the matrix core and the vector ALU of one SIMD overlap: the matrix
+//     and the vector work of one wave and key block, each alone, split over
+//     two waves of a SIMD (the fast kernel's ping-pong) or interleaved in one
+//     wave per SIMD.
 // Every kernel bounds-checks its index against n.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -266,6 +270,191 @@ static int grid_for(int64_t items, int per_block)
     return (int)((items + per_block - 1) / per_block);
 }
 
+// ---- co-execution of the matrix core and the vector ALU ----
+// Matrix stream, one wave's matrix work per 128-key block of the fast kernel
+// (d = 128, bf16 scores): 32 bf16 32x32x16 MFMAs (S^T) and 8 FP8 32x32x64
+// MFMAs (P.V), 1536 matrix-core cycles at the documented rates.
+__device__ __forceinline__ void coexec_mfma(f32x16 (&acc)[4], f32x16 (&o)[4], bf16x8 a, bf16x8 b, i32x8 a8,
+                                            i32x8 b8)
+{
+#pragma unroll
+    for (int kk = 0; kk < 8; ++kk)
+#pragma unroll
+        for (int kt = 0; kt < 4; ++kt)
+            acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[kt], 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+        o[i & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, o[i & 3], 0, 0, 0, 0, 0, 0);
+}
+
+// Vector stream, the instruction mix of the softmax of one wave and block:
+// a maximum over 64 values (v_max3 pairs), 64 FMAs, 64 exp2, 64 adds (the
+// row sum), 32 scaled E4M3 pair converts and 64 multiplies (the rescale of O).
+// Every value feeds the next iteration, so no work can be hoisted or dropped.
+__device__ __forceinline__ void coexec_rescale(float (&ov)[64], float alpha)
+{
+#pragma unroll
+    for (int i = 0; i < 64; ++i)
+        ov[i] *= alpha;
+}
+__device__ __forceinline__ void coexec_rescale(f32x16 (&ov)[4], float alpha)
+{
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            ov[i][r] *= alpha;
+}
+template <typename OV>
+__device__ __forceinline__ void coexec_valu(float (&x)[64], OV& ov, uint32_t (&pk)[16], float& l, float& mc)
+{
+    float mx = x[0];
+#pragma unroll
+    for (int i = 1; i < 63; i += 2)
+        mx = __builtin_fmaxf(__builtin_fmaxf(mx, x[i]), x[i + 1]);
+    mx = __builtin_fmaxf(mx, x[63]);
+    const float alpha = __builtin_amdgcn_exp2f(mc - mx);
+    mc = mx;
+#pragma unroll
+    for (int i = 0; i < 64; ++i)
+        x[i] = __builtin_fmaf(x[i], 0.75f, -mx);
+#pragma unroll
+    for (int i = 0; i < 64; ++i)
+        x[i] = __builtin_amdgcn_exp2f(x[i]);
+    float l0 = 0.f, l1 = 0.f, l2 = 0.f, l3 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 64; i += 4) {
+        l0 += x[i];
+        l1 += x[i + 1];
+        l2 += x[i + 2];
+        l3 += x[i + 3];
+    }
+    l = l * alpha + ((l0 + l1) + (l2 + l3));
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        s16x2 w = __builtin_bit_cast(s16x2, pk[i]);
+        w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, x[4 * i], x[4 * i + 1], 0.00390625f, false);
+        w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, x[4 * i + 2], x[4 * i + 3], 0.00390625f, true);
+        pk[i] = __builtin_bit_cast(uint32_t, w);
+    }
+    coexec_rescale(ov, alpha);
+}
+
+// One stream per wave (kind 0: matrix, 1: vector) for `iters` iterations;
+// returns a checksum of the stream's final state and the s_memtime cycles.
+template <int KIND>
+__device__ float coexec_run(int iters, int lane, unsigned long long& cyc)
+{
+    unsigned long long t0, t1;
+    float sum = 0.f;
+    if constexpr (KIND == 0) {
+        f32x16 acc[4], o[4];
+        for (int i = 0; i < 4; ++i)
+            for (int r = 0; r < 16; ++r) {
+                acc[i][r] = 0.f;
+                o[i][r] = 0.f;
+            }
+        bf16x8 a, b;
+        i32x8 a8, b8;
+        for (int i = 0; i < 8; ++i) {
+            a[i] = (__bf16)(0.0078125f * (float)((lane + i) & 7));
+            b[i] = (__bf16)(0.0078125f * (float)(i + 1));
+            a8[i] = 0x30303030;     // E4M3 0.5 in every byte
+            b8[i] = 0x20202020;     // E4M3 0.0625
+        }
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+        for (int it = 0; it < iters; ++it)
+            coexec_mfma(acc, o, a, b, a8, b8);
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
+        for (int i = 0; i < 4; ++i)
+            for (int r = 0; r < 16; ++r)
+                sum += acc[i][r] + o[i][r];
+    } else {
+        float x[64], ov[64];
+        uint32_t pk[16];
+        for (int i = 0; i < 64; ++i) {
+            x[i] = -0.015625f * (float)((i + lane) & 31);
+            ov[i] = 1.f;
+        }
+        for (int i = 0; i < 16; ++i)
+            pk[i] = 0;
+        float l = 0.f, mc = 0.f;
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+        for (int it = 0; it < iters; ++it)
+            coexec_valu(x, ov, pk, l, mc);
+        asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
+        sum = l;
+        for (int i = 0; i < 64; ++i)
+            sum += x[i] + ov[i];
+        for (int i = 0; i < 16; ++i)
+            sum += (float)(pk[i] & 0xFFu);
+    }
+    cyc = t1 - t0;
+    return sum;
+}
+
+// layout 0: waves 0-3 (one per SIMD) run the matrix stream; layout 1: waves 0-3
+// run the vector stream; layout 2: 8 waves, wave w and wave w + 4 share SIMD
+// w, waves 0-3 run the matrix stream and waves 4-7 the vector stream.
+// cycles[wg * 8 + wave] gets the wave's cycles, sink[wg * 512 + thread] its checksum.
+__global__ void __launch_bounds__(512) k_coexec(int iters, int layout, unsigned long long* cycles, float* sink)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int kind = layout == 2 ? (w < 4 ? 0 : 1) : layout;
+    unsigned long long cyc = 0;
+    const float sum = kind == 0 ? coexec_run<0>(iters, lane, cyc) : coexec_run<1>(iters, lane, cyc);
+    sink[blockIdx.x * 512 + threadIdx.x] = sum;
+    if (lane == 0)
+        cycles[blockIdx.x * 8 + w] = cyc;
+}
+
+// layout 3: waves 0-3, one per SIMD with the whole register file, each run both
+// streams per iteration (the compiler interleaves them); the vector stream's
+// multiplies rescale the P.V accumulators, as in the attention kernels
+__global__ void __launch_bounds__(512) k_coexec_one(int iters, unsigned long long* cycles, float* sink)
+{
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    f32x16 acc[4], o[4];
+    for (int i = 0; i < 4; ++i)
+        for (int r = 0; r < 16; ++r) {
+            acc[i][r] = 0.f;
+            o[i][r] = 0.f;
+        }
+    bf16x8 a, b;
+    i32x8 a8, b8;
+    for (int i = 0; i < 8; ++i) {
+        a[i] = (__bf16)(0.0078125f * (float)((lane + i) & 7));
+        b[i] = (__bf16)(0.0078125f * (float)(i + 1));
+        a8[i] = 0x30303030;
+        b8[i] = 0x20202020;
+    }
+    float x[64];
+    uint32_t pk[16];
+    for (int i = 0; i < 64; ++i)
+        x[i] = -0.015625f * (float)((i + lane) & 31);
+    for (int i = 0; i < 16; ++i)
+        pk[i] = 0;
+    float l = 0.f, mc = 0.f;
+    unsigned long long t0, t1;
+    asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+    for (int it = 0; it < iters; ++it) {
+        coexec_mfma(acc, o, a, b, a8, b8);
+        coexec_valu(x, o, pk, l, mc);
+    }
+    asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
+    float sum = l;
+    for (int i = 0; i < 4; ++i)
+        for (int r = 0; r < 16; ++r)
+            sum += acc[i][r] + o[i][r];
+    for (int i = 0; i < 64; ++i)
+        sum += x[i];
+    for (int i = 0; i < 16; ++i)
+        sum += (float)(pk[i] & 0xFFu);
+    sink[blockIdx.x * 512 + threadIdx.x] = sum;
+    if (lane == 0)
+        cycles[blockIdx.x * 8 + w] = t1 - t0;
+}
+
 extern "C" {
 
 int probe_cvt_range(uint32_t lo, int64_t n, uint8_t* out, void* stream)
@@ -347,6 +536,21 @@ int probe_mfma(int which, const void* A, const void* B, float* D, void* stream)
         hipLaunchKernelGGL(k_mfma_f32, dim3(1), dim3(64), 0, s, (const float*)A, (const float*)B, D);
     else
         return -1;
+    return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+// cycles: blocks * 8 entries, sink: blocks * 512 floats (layouts 0, 1 and 3
+// write waves 0-3 only)
+int probe_coexec(int blocks, int iters, int layout, unsigned long long* cycles, float* sink, void* stream)
+{
+    if (blocks <= 0 || iters <= 0 || layout < 0 || layout > 3 || !cycles || !sink)
+        return -1;
+    hipStream_t s = (hipStream_t)stream;
+    if (layout == 3)
+        hipLaunchKernelGGL(k_coexec_one, dim3(blocks), dim3(256), 0, s, iters, cycles, sink);
+    else
+        hipLaunchKernelGGL(k_coexec, dim3(blocks), dim3(layout == 2 ? 512 : 256), 0, s, iters, layout, cycles,
+                           sink);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

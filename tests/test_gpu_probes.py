@@ -179,6 +179,47 @@ def test_lds_read_rate(probes):
                 assert np.all(got[:, w, :] == want[None, :]), w
 
 
+
+def test_mfma_valu_coexec(probes):
+    """How one SIMD's matrix core and vector ALU overlap, in shader cycles per
+    iteration (s_memtime, median over 256 workgroups of the slowest wave of a
+    kind).  The matrix stream is one wave's MFMA work per 128-key block of the
+    fast kernel (32 bf16 32x32x16 + 8 FP8 32x32x64, 1536 cycles at the
+    documented rates); the vector stream is the softmax's instruction mix.
+    Layouts: each stream alone (one wave per SIMD); the fast kernel's ping-pong
+    (an MFMA wave and a vector wave on every SIMD); and one wave per SIMD that
+    runs both streams.  The matrix stream alone pins the 1536-cycle cost; the
+    rest is reported (the vector wave's slowdown beside the MFMA wave is the
+    co-execution cost the fast kernel's phases pay)."""
+    blocks, iters = 256, 1001
+    cyc = torch.zeros(blocks * 8, dtype=torch.int64, device="cuda")
+    sink = torch.zeros(blocks * 512, dtype=torch.float32, device="cuda")
+    s = torch.cuda.current_stream()
+    res = {}
+    for layout in range(4):
+        cyc.zero_()
+        assert probes.probe_coexec(blocks, 8, layout, cyc.data_ptr(), sink.data_ptr(), s.cuda_stream) == 0
+        assert probes.probe_coexec(blocks, iters, layout, cyc.data_ptr(), sink.data_ptr(),
+                                   s.cuda_stream) == 0
+        torch.cuda.synchronize()
+        c = cyc.cpu().numpy().reshape(blocks, 8).astype(np.float64) / iters
+        nw = 8 if layout == 2 else 4
+        assert np.all(c[:, :nw] > 0)
+        y = sink.cpu().numpy().reshape(blocks, 512)[:, :64 * nw]
+        assert np.all(np.isfinite(y))
+        res[layout] = (float(np.median(c[:, :4].max(axis=1))),
+                       float(np.median(c[:, 4:8].max(axis=1))) if layout == 2 else None)
+    mfma, valu = res[0][0], res[1][0]
+    split_m, split_v = res[2]
+    one = res[3][0]
+    print(f"matrix stream alone {mfma:.0f} cycles/iteration, vector stream alone {valu:.0f}; "
+          f"ping-pong: MFMA wave {split_m:.0f}, vector wave {split_v:.0f} "
+          f"({100 * (split_v / valu - 1):+.1f} % beside the MFMA wave); one wave running both {one:.0f}",
+          flush=True)
+    assert 1536 * 0.98 < mfma < 1536 * 1.1
+    assert split_m >= 0.95 * mfma and split_v >= 0.95 * valu
+    assert one >= 0.95 * max(mfma, valu)
+
 def test_mfma_bf16_layout(probes):
     rng = np.random.default_rng(8)
     A = rng.integers(-8, 9, (32, 16)).astype(np.float32)
