@@ -96,6 +96,7 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     __shared__ float tab[NW][32];     // pass 1: each wave's row maxima
     __shared__ float lsh[NW][32];     // merge: each wave's l, at the final maximum
     __shared__ uint32_t csh[32][3];   // merge: counts
+    __shared__ float rmax[PHASE == 2 ? 8 * NW : 1][32];   // PHASE 2: the maxima of every range
 
     // workgroup -> (tile unit, part cidx of C); the C workgroups of a unit are
     // consecutive logical indices inside one XCD's contiguous range
@@ -182,6 +183,10 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt)
                 load_tile(a[kt], kt);
+            // every load of the block is requested before the first MFMA waits
+            // (the compiler would otherwise issue each load next to its MFMA,
+            // one HBM round trip per k-step)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
                 s[kt] = mfma_qk(a[kt][0], 0, f32x16{});
@@ -196,10 +201,12 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
             for (int kt = 0; kt < KT; ++kt) {
                 if (kt + 1 < KT)
                     load_tile(a[(kt + 1) & 1], kt + 1);
+                __builtin_amdgcn_sched_barrier(0);
                 s[kt] = mfma_qk(a[kt & 1][0], 0, f32x16{});
 #pragma unroll
                 for (int kk = 1; kk < DK; ++kk)
                     s[kt] = mfma_qk(a[kt & 1][kk], kk, s[kt]);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
     };
@@ -252,19 +259,32 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
             m_final = fmax_f(m_final, tab[v][n]);
         }
     } else {
-        // the maxima of every range of the tile, from the PHASE 1 launch, read
-        // eight ranges (one part) per round
-        const float* mx = p.ws_max + (size_t)unit * R * 32 + n;
+        // the maxima of every range of the tile, from the PHASE 1 launch: the
+        // workgroup stages all R x 32 of them (R <= 8 NW) in LDS with one round
+        // of loads, then each wave reduces its prefix and the total, eight
+        // ranges per round
+        const float* mx = p.ws_max + (size_t)unit * R * 32;
+        constexpr int PER = 8 * NW * 32 / (64 * NW);
+        float t[PER];
+#pragma unroll
+        for (int q = 0; q < PER; ++q) {
+            const int e = tid + 64 * NW * q;
+            t[q] = e < R * 32 ? mx[e] : -INFINITY;
+        }
+#pragma unroll
+        for (int q = 0; q < PER; ++q)
+            rmax[(tid + 64 * NW * q) / 32][(tid + 64 * NW * q) % 32] = t[q];
+        __syncthreads();
         for (int cc = 0; cc < C; ++cc) {
-            float t[NW];
+            float v[NW];
 #pragma unroll
-            for (int v = 0; v < NW; ++v)
-                t[v] = mx[32 * (cc * NW + v)];
+            for (int u = 0; u < NW; ++u)
+                v[u] = rmax[cc * NW + u][n];
 #pragma unroll
-            for (int v = 0; v < NW; ++v) {
-                if (cc * NW + v < g)
-                    m_start = fmax_f(m_start, t[v]);
-                m_final = fmax_f(m_final, t[v]);
+            for (int u = 0; u < NW; ++u) {
+                if (cc * NW + u < g)
+                    m_start = fmax_f(m_start, v[u]);
+                m_final = fmax_f(m_final, v[u]);
             }
         }
     }
@@ -297,13 +317,25 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     // the start of the block, so it travels with the K loads of the scores;
     // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
     // Nk - 1; their P is 0.
+    // (V_RPI is a multiple of 256 / VROW and VCPR / 2 divides V_RPI / (256 /
+    // VROW), so the swizzle of row i V_RPI + l / VCPR does not depend on i: a
+    // block inside the cache takes one lane offset and a uniform row step)
+    static_assert(V_RPI % (256 / VROW) == 0 && (V_RPI / (256 / VROW)) % (VCPR / 2) == 0,
+                  "the V swizzle repeats every round");
+    const uint32_t v_voff = (uint32_t)((lane / VCPR) * VROW + 16 * ((lane % VCPR) ^ vswz(lane / VCPR)));
     auto issue_v = [&](int j) __attribute__((always_inline)) {
         const int t0 = j * BC;
+        if (t0 + BC <= Nk) {
 #pragma unroll
-        for (int i = 0; i < V_NI; ++i) {
-            const int rv = i * V_RPI + lane / VCPR;
-            const int lc = (lane % VCPR) ^ vswz(rv);
-            g2lds(Vg, (uint32_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc, vst + 1024 * i);
+            for (int i = 0; i < V_NI; ++i)
+                g2lds(Vg + (size_t)(t0 + i * V_RPI) * VROW, v_voff, vst + 1024 * i);
+        } else {
+#pragma unroll
+            for (int i = 0; i < V_NI; ++i) {
+                const int rv = i * V_RPI + lane / VCPR;
+                const int lc = (lane % VCPR) ^ vswz(rv);
+                g2lds(Vg, (uint32_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc, vst + 1024 * i);
+            }
         }
     };
 
