@@ -36,7 +36,7 @@ def lib() -> ctypes.CDLL:
         L.probe_cvt_scaled_vec.argtypes = [P, P, I64, P, P]
         L.probe_exp2_rate.argtypes = [I, I, P, P]
         L.probe_lds_rate.argtypes = [I, I, I, I, I, P, P, P, P]
-        L.probe_coexec.argtypes = [I, I, I, P, P, P]
+        L.probe_coexec.argtypes = [I, I, I, I, P, P, P]
         for f in (L.probe_cvt_range, L.probe_cvt_list, L.probe_exp2, L.probe_mfma,
                   L.probe_mfma_fp8_scaled, L.probe_cvt_scaled_vec, L.probe_exp2_rate,
                   L.probe_lds_rate, L.probe_coexec):

@@ -16,7 +16,7 @@
 //   - how the matrix core and the vector ALU of one SIMD overlap: the matrix
 //     and the vector work of one wave and key block, each alone, split over
 //     two waves of a SIMD (the fast kernel's ping-pong) or interleaved in one
-//     wave per SIMD.
+//     wave per SIMD, and what each MFMA shape costs the vector wave.
 // Every kernel bounds-checks its index against n.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -271,20 +271,38 @@ static int grid_for(int64_t items, int per_block)
 }
 
 // ---- co-execution of the matrix core and the vector ALU ----
-// Matrix stream, one wave's matrix work per 128-key block of the fast kernel
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+// Matrix streams, each 1536 matrix-core cycles at the documented rates.
+// pattern 0: one wave's matrix work per 128-key block of the fast kernel
 // (d = 128, bf16 scores): 32 bf16 32x32x16 MFMAs (S^T) and 8 FP8 32x32x64
-// MFMAs (P.V), 1536 matrix-core cycles at the documented rates.
-__device__ __forceinline__ void coexec_mfma(f32x16 (&acc)[4], f32x16 (&o)[4], bf16x8 a, bf16x8 b, i32x8 a8,
-                                            i32x8 b8)
+// MFMAs (P.V); 1: 24 FP8 32x32x64; 2: 48 bf16 32x32x16; 3: 96 bf16 16x16x32
+// (four accumulators in rotation in every pattern)
+template <int PAT>
+__device__ __forceinline__ void coexec_mfma(f32x16 (&acc)[4], f32x16 (&o)[4], f32x4 (&q)[4], bf16x8 a, bf16x8 b,
+                                            i32x8 a8, i32x8 b8)
 {
+    if constexpr (PAT == 0) {
 #pragma unroll
-    for (int kk = 0; kk < 8; ++kk)
+        for (int kk = 0; kk < 8; ++kk)
 #pragma unroll
-        for (int kt = 0; kt < 4; ++kt)
-            acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[kt], 0, 0, 0);
+            for (int kt = 0; kt < 4; ++kt)
+                acc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[kt], 0, 0, 0);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-        o[i & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, o[i & 3], 0, 0, 0, 0, 0, 0);
+        for (int i = 0; i < 8; ++i)
+            o[i & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, o[i & 3], 0, 0, 0, 0, 0, 0);
+    } else if constexpr (PAT == 1) {
+#pragma unroll
+        for (int i = 0; i < 24; ++i)
+            o[i & 3] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, o[i & 3], 0, 0, 0, 0, 0, 0);
+    } else if constexpr (PAT == 2) {
+#pragma unroll
+        for (int i = 0; i < 48; ++i)
+            acc[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i & 3], 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 96; ++i)
+            q[i & 3] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, q[i & 3], 0, 0, 0);
+    }
 }
 
 // Vector stream, the instruction mix of the softmax of one wave and block:
@@ -342,17 +360,19 @@ __device__ __forceinline__ void coexec_valu(float (&x)[64], OV& ov, uint32_t (&p
 
 // One stream per wave (kind 0: matrix, 1: vector) for `iters` iterations;
 // returns a checksum of the stream's final state and the s_memtime cycles.
-template <int KIND>
+template <int KIND, int PAT>
 __device__ float coexec_run(int iters, int lane, unsigned long long& cyc)
 {
     unsigned long long t0, t1;
     float sum = 0.f;
     if constexpr (KIND == 0) {
         f32x16 acc[4], o[4];
+        f32x4 q[4];
         for (int i = 0; i < 4; ++i)
             for (int r = 0; r < 16; ++r) {
                 acc[i][r] = 0.f;
                 o[i][r] = 0.f;
+                q[i][r & 3] = 0.f;
             }
         bf16x8 a, b;
         i32x8 a8, b8;
@@ -364,11 +384,11 @@ __device__ float coexec_run(int iters, int lane, unsigned long long& cyc)
         }
         asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
         for (int it = 0; it < iters; ++it)
-            coexec_mfma(acc, o, a, b, a8, b8);
+            coexec_mfma<PAT>(acc, o, q, a, b, a8, b8);
         asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
         for (int i = 0; i < 4; ++i)
             for (int r = 0; r < 16; ++r)
-                sum += acc[i][r] + o[i][r];
+                sum += acc[i][r] + o[i][r] + q[i][r & 3];
     } else {
         float x[64], ov[64];
         uint32_t pk[16];
@@ -396,13 +416,15 @@ __device__ float coexec_run(int iters, int lane, unsigned long long& cyc)
 // layout 0: waves 0-3 (one per SIMD) run the matrix stream; layout 1: waves 0-3
 // run the vector stream; layout 2: 8 waves, wave w and wave w + 4 share SIMD
 // w, waves 0-3 run the matrix stream and waves 4-7 the vector stream.
-// cycles[wg * 8 + wave] gets the wave's cycles, sink[wg * 512 + thread] its checksum.
+// The matrix stream is pattern PAT.  cycles[wg * 8 + wave] gets the wave's
+// cycles, sink[wg * 512 + thread] its checksum.
+template <int PAT>
 __global__ void __launch_bounds__(512) k_coexec(int iters, int layout, unsigned long long* cycles, float* sink)
 {
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int kind = layout == 2 ? (w < 4 ? 0 : 1) : layout;
     unsigned long long cyc = 0;
-    const float sum = kind == 0 ? coexec_run<0>(iters, lane, cyc) : coexec_run<1>(iters, lane, cyc);
+    const float sum = kind == 0 ? coexec_run<0, PAT>(iters, lane, cyc) : coexec_run<1, 0>(iters, lane, cyc);
     sink[blockIdx.x * 512 + threadIdx.x] = sum;
     if (lane == 0)
         cycles[blockIdx.x * 8 + w] = cyc;
@@ -437,8 +459,9 @@ __global__ void __launch_bounds__(512) k_coexec_one(int iters, unsigned long lon
     float l = 0.f, mc = 0.f;
     unsigned long long t0, t1;
     asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t0) :: "memory");
+    f32x4 q[4] = {};
     for (int it = 0; it < iters; ++it) {
-        coexec_mfma(acc, o, a, b, a8, b8);
+        coexec_mfma<0>(acc, o, q, a, b, a8, b8);
         coexec_valu(x, o, pk, l, mc);
     }
     asm volatile("s_memtime %0\n\ts_waitcnt lgkmcnt(0)" : "=s"(t1) :: "memory");
@@ -540,17 +563,25 @@ int probe_mfma(int which, const void* A, const void* B, float* D, void* stream)
 }
 
 // cycles: blocks * 8 entries, sink: blocks * 512 floats (layouts 0, 1 and 3
-// write waves 0-3 only)
-int probe_coexec(int blocks, int iters, int layout, unsigned long long* cycles, float* sink, void* stream)
+// write waves 0-3 only); pattern: the matrix stream of layouts 0 and 2 (0-3;
+// layout 3 runs pattern 0)
+int probe_coexec(int blocks, int iters, int layout, int pattern, unsigned long long* cycles, float* sink,
+                 void* stream)
 {
-    if (blocks <= 0 || iters <= 0 || layout < 0 || layout > 3 || !cycles || !sink)
+    if (blocks <= 0 || iters <= 0 || layout < 0 || layout > 3 || pattern < 0 || pattern > 3 || !cycles || !sink)
         return -1;
     hipStream_t s = (hipStream_t)stream;
+    const dim3 blk(layout == 2 ? 512 : 256);
     if (layout == 3)
         hipLaunchKernelGGL(k_coexec_one, dim3(blocks), dim3(256), 0, s, iters, cycles, sink);
+    else if (pattern == 0)
+        hipLaunchKernelGGL(k_coexec<0>, dim3(blocks), blk, 0, s, iters, layout, cycles, sink);
+    else if (pattern == 1)
+        hipLaunchKernelGGL(k_coexec<1>, dim3(blocks), blk, 0, s, iters, layout, cycles, sink);
+    else if (pattern == 2)
+        hipLaunchKernelGGL(k_coexec<2>, dim3(blocks), blk, 0, s, iters, layout, cycles, sink);
     else
-        hipLaunchKernelGGL(k_coexec, dim3(blocks), dim3(layout == 2 ? 512 : 256), 0, s, iters, layout, cycles,
-                           sink);
+        hipLaunchKernelGGL(k_coexec<3>, dim3(blocks), blk, 0, s, iters, layout, cycles, sink);
     return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 
