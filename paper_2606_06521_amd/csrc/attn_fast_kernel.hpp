@@ -142,10 +142,9 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
     constexpr int V_NI = V_BYTES / 4096;
     static_assert(K_NI >= 1 && V_NI >= 1, "stage smaller than one round of loads");
 
-    __shared__ __attribute__((aligned(1024))) uint8_t Ks0[PAIR ? 1 : K_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Ks1[PAIR ? 1 : K_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Vs0[PAIR ? 1 : V_BYTES];
-    __shared__ __attribute__((aligned(1024))) uint8_t Vs1[PAIR ? 1 : V_BYTES];
+    // 256-row schedule: K stages 0 and 1, then V stages 0 and 1, contiguous
+    // (the output tile is staged in [K_BYTES, K_BYTES + 32 KB) at the end)
+    __shared__ __attribute__((aligned(1024))) uint8_t Sst[PAIR ? 1 : 2 * (K_BYTES + V_BYTES)];
     // PAIR: two K and two V stages (stage r at Kst + r K_BYTES, Vst +
     // r V_BYTES), and the running maximum of each row (row group w & 3, row n)
     // after the last block processed
@@ -618,7 +617,7 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             }
         } else {
             if (grp == 0)
-                load_k(Ks0, jof(0));
+                load_k(Sst, jof(0));
         }
         // Q fragments and the first K stage are complete after this point; the
         // compiler sees the wait (it tracks no outstanding loads in the loop)
@@ -706,6 +705,10 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
                     wait_loads();
                 __syncthreads();
             };
+            uint8_t* const Ks0 = Sst;
+            uint8_t* const Ks1 = Sst + K_BYTES;
+            uint8_t* const Vs0 = Sst + 2 * K_BYTES;
+            uint8_t* const Vs1 = Sst + 2 * K_BYTES + V_BYTES;
             for (int k = 0; k <= nb; k += 2) {
                 iteration(k, Ks0, Ks1, Vs0, Vs1);
                 if (k + 1 <= nb)
@@ -781,9 +784,48 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
             cnt1 += other_half_u32(cnt1);
             cnt2 += other_half_u32(cnt2);
         }
+        // Output through LDS (256-row schedule, d = 128): each wave stages its
+        // 32 rows x 32 columns per round (4 KB, wave w at K_BYTES + 4096 w, past
+        // stage K 0, the only stage the next tile writes before its first
+        // barrier) and stores 8 whole 128-byte row segments per instruction,
+        // instead of 32 rows x 32 bytes straight from the accumulator layout.
+        constexpr bool STAGED_OUT = !PAIR && D == 128 && K_BYTES + V_BYTES >= 8 * 4096;
+        if constexpr (STAGED_OUT) {
+            if (p.out) {
+                const float inv = p.v_descale / (S * ell_row);
+                // per-lane LDS addresses, materialised here (not hoisted out of
+                // the tile loop): write chunk c = 2 r4 + h of row n at
+                // 16 (c ^ (n & 7)) = wa ^ 32 r4; read row 8 i + rr, chunk cc at ra + 1024 i
+                const uint32_t base_w = lds_addr(Sst) + K_BYTES + 4096u * (uint32_t)w;
+                const uint32_t x = (uint32_t)n & 7u;
+                const uint32_t wa = lds_base(base_w + 128u * (uint32_t)n + 16u * ((uint32_t)h ^ (x & 1u)) +
+                                             32u * (x >> 1));
+                const uint32_t rr = (uint32_t)lane >> 3, cc = (uint32_t)lane & 7u;
+                const uint32_t ra = lds_base(base_w + 128u * rr + 16u * (cc ^ rr));
+                float* const orow0 = p.out + ((size_t)bh * N + wrow0 + rr) * D + 4 * cc;
+#pragma unroll
+                for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+                    for (int r4 = 0; r4 < 4; ++r4) {
+                        f32x4 v4;
+                        v4[0] = o[dt][4 * r4 + 0] * inv;
+                        v4[1] = o[dt][4 * r4 + 1] * inv;
+                        v4[2] = o[dt][4 * r4 + 2] * inv;
+                        v4[3] = o[dt][4 * r4 + 3] * inv;
+                        *reinterpret_cast<__attribute__((address_space(3))) f32x4*>((uintptr_t)(wa ^ (32u * r4))) = v4;
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const f32x4 v4 = lds_load<f32x4>(ra + 1024u * i);
+                        if (wrow0 + 8 * i + (int)rr < N)
+                            *reinterpret_cast<f32x4*>(orow0 + (size_t)8 * i * D + 32 * dt) = v4;
+                    }
+                }
+            }
+        }
         if (row < N) {
             const size_t flat = (size_t)bh * N + row;
-            if (p.out) {
+            if (!STAGED_OUT && p.out) {
                 const float inv = p.v_descale / (S * ell_row);
                 float* orow = p.out + flat * D;
 #pragma unroll
