@@ -81,6 +81,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-ms", type=float, default=100.0,
+                    help="after the warm-up steps, keep running untimed steps until this much wall time "
+                         "has passed since the first warm-up step (the GPU clock's ramp under load; "
+                         "reported as settle_ms / settle_steps; 0 turns it off)")
     ap.add_argument("--workload", default=None)
     ap.add_argument("--order", default=None, choices=[None, "forward", "reverse"])
     ap.add_argument("--S", type=float, default=None)
@@ -226,9 +230,21 @@ def main() -> int:
         if st != A.ATTN_OK:
             raise A.AttnError(st)
 
+    t_w0 = time.perf_counter()
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    # The GPU's clock ramps up over the first tens of milliseconds of sustained
+    # load: in kernel traces of this step the first launches take up to 1.35x
+    # the settled time and the time keeps falling for about 25 launches.
+    # Untimed steps continue until settle_ms have passed since the first
+    # warm-up step, so the K timed steps see the settled clock.
+    settle_steps = 0
+    while (time.perf_counter() - t_w0) * 1e3 < args.settle_ms:
+        for _ in range(4):
+            step()
+        torch.cuda.synchronize()
+        settle_steps += 4
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     t0 = time.perf_counter()
@@ -274,6 +290,8 @@ def main() -> int:
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "settle_ms": args.settle_ms,
+        "settle_steps": settle_steps,
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -530,8 +548,15 @@ def _report_run(label, w, inp, dev, S, order, rows, keys_s, ref, denom, peak, re
         if st != A.ATTN_OK:
             raise A.AttnError(st)
 
+    # warm-up launches, then untimed ones until the clock has settled (as in
+    # the bench line: 100 ms after the first warm-up launch)
+    t_w0 = time.perf_counter()
     for _ in range(warm):
         step()
+    torch.cuda.synchronize()
+    while (time.perf_counter() - t_w0) * 1e3 < 100.0:
+        step()
+        torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(reps)]
     for s_ev, e_ev in ev:
