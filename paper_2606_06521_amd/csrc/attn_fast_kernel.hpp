@@ -1,6 +1,8 @@
 // The fast kernel (template): bfloat16 Q and K (QK8 = false) or OCP E4M3 Q
 // and K (QK8 = true), OCP E4M3 V; the E4M3 P bytes feed the FP8 MFMA.
-// Instantiated by attn_fast.hip (bf16 Q/K) and attn_fast_qk8.hip (E4M3 Q/K).
+// Instantiated through attn_fast_dispatch.hpp by attn_fast.hip and
+// attn_fast_qk8.hip (256-row tiles) and attn_fast_pair.hip and
+// attn_fast_qk8_pair.hip (128-row tiles, PAIR), bf16 and E4M3 Q/K.
 //
 // Algorithm 1 per query row with the kernel semantics of Sec. 6.1, one KV block
 // of BC keys per iteration, in forward or reverse block order:
@@ -38,6 +40,10 @@
 // and the transposed V reads of a lane group fall in distinct banks.  With
 // that layout a loading lane's HBM offset is a per-lane constant plus a
 // per-block scalar, so issuing a load costs no vector instructions.
+//
+// Output (256-row tiles, d = 128): the tile's O goes through the idle K/V
+// stages, so each store writes whole 128-byte row segments instead of the
+// accumulator layout's 32 rows x 32 bytes.
 #pragma once
 
 #include "attn_common.hpp"
