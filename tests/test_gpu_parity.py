@@ -126,6 +126,23 @@ def test_edge_lengths(N, mode):
         compare(inp, gpu, mode, 256.0, order, causal, 64, label=label)
 
 
+@pytest.mark.parametrize("N", [255, 257, 513])
+@pytest.mark.parametrize("mode", ["fast", "fp8qk"])
+def test_edge_lengths_block128(N, mode):
+    # d = 128 with 128-key blocks: the fast kernel's output tile goes through
+    # LDS on the 256-row schedule; these lengths leave a last tile with one
+    # ragged wave (255), one valid row (257) or one valid row past two full
+    # tiles (513), and waves with no valid row at all
+    fmt = {"fast": "bf16_e4m3", "fp8qk": "e4m3"}[mode]
+    inp = make_inputs(1, 2, 1, N, 128, fmt=fmt, delta=9.0, seed=700 + N)
+    dev = to_device(inp)
+    for causal, order, tile in itertools.product([False, True], ["forward", "reverse"], TILES):
+        label = f"{mode} N={N} bkv=128 causal={causal} {order} tile={tile}"
+        log(label)
+        gpu = run_gpu(dev, mode, 256.0, order, causal, 128, tile=tile)
+        compare(inp, gpu, mode, 256.0, order, causal, 128, label=label)
+
+
 def test_empty_problem_is_a_noop():
     from paper_2606_06521_amd import attn_fp8 as A
     st = A.attn_fp8_fwd(None, None, None, None, None, 1, 4, 2, 0, 128, 1, 128, 1, 256.0, 1,
