@@ -126,7 +126,8 @@ enum {
 enum {
     ATTN_OK = 0,
     ATTN_ERR_INVALID_ARG = -1, /* null pointer, bad shape, S not finite/positive, ... */
-    ATTN_ERR_UNSUPPORTED = -2, /* valid but not built: d or block_kv outside {64,128} */
+    ATTN_ERR_UNSUPPORTED = -2, /* valid but not built: d or block_kv outside {64,128},
+                                  more than 2^30 keys per (batch, head) */
     ATTN_ERR_HIP = -3,         /* the HIP runtime rejected the launch */
     ATTN_ERR_SCRATCH = -4      /* attn_fp8_fwd_kv_noalloc: shape needs more than its scratch */
 };
@@ -138,8 +139,9 @@ enum {
  *   lse       device float32 [B][Hq][N]; may be NULL.
  *   B, Hq, Hkv, N, d
  *             batch, query heads, KV heads (Hq % Hkv == 0), sequence length,
- *             head dimension (64 or 128).  N may be any value >= 0; B*Hq*N == 0
- *             is a no-op (pointers are then not inspected).
+ *             head dimension (64 or 128).  N may be any value in [0, 2^30]
+ *             (beyond: ATTN_ERR_UNSUPPORTED); B*Hq*N == 0 is a no-op
+ *             (pointers are then not inspected).
  *   causal    0 or 1.
  *   block_kv  KV block size B of Algorithm 1: 64 or 128.  It is the granularity
  *             of the running-maximum update and therefore part of the result.
@@ -234,7 +236,8 @@ int attn_fp8_p_underflow_count_descaled(const void* q, const void* k, const void
  *   workspace_bytes  its size; with a non-NULL workspace it must be at least
  *                    what attn_fp8_kv_workspace_bytes reports for the same
  *                    shape on the current device, else ATTN_ERR_INVALID_ARG.
- * Nq > Nk returns ATTN_ERR_INVALID_ARG; other arguments and return codes as
+ * Nq > Nk returns ATTN_ERR_INVALID_ARG, Nk > 2^30 ATTN_ERR_UNSUPPORTED; other
+ * arguments and return codes as
  * for the descaled entry points.
  */
 int attn_fp8_fwd_kv(const void* q, const void* k, const void* v, float* out, float* lse,

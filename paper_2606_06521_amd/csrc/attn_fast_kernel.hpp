@@ -219,6 +219,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
         // bits and the swizzle does not depend on it).  V likewise with
         // key = row.  Keys past the end of the sequence (only in a ragged last
         // block) read row Nk-1: they are masked to P = 0 before they can contribute.
+        // The per-lane offset is taken from the block's first row, so it stays
+        // below 2^32 for any number of keys.
         const int wl = w & 3;
         int k_key_l, v_key_l;
         uint32_t k_chunk_l, v_chunk_l;
@@ -243,7 +245,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
 #pragma unroll
                 for (int it = 0; it < K_NI; ++it) {
                     const int key = min(t0 + krow_key(4 * K_RPI * it) + k_key_l, Nk - 1);
-                    g2lds16(Kg, (uint32_t)key * KROW + k_chunk_l, lds_addr(dst) + (wl + 4 * it) * 1024);
+                    g2lds16(Kg + (size_t)t0 * KROW, (uint32_t)(key - t0) * KROW + k_chunk_l,
+                            lds_addr(dst) + (wl + 4 * it) * 1024);
                 }
             }
         };
@@ -257,7 +260,8 @@ __global__ void __launch_bounds__(512) fast_kernel(Params p)
 #pragma unroll
                 for (int it = 0; it < V_NI; ++it) {
                     const int key = min(t0 + 4 * V_RPI * it + v_key_l, Nk - 1);
-                    g2lds16(Vg, (uint32_t)key * VROW + v_chunk_l, lds_addr(dst) + (wl + 4 * it) * 1024);
+                    g2lds16(Vg + (size_t)t0 * VROW, (uint32_t)(key - t0) * VROW + v_chunk_l,
+                            lds_addr(dst) + (wl + 4 * it) * 1024);
                 }
             }
         };

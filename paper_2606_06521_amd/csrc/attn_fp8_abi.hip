@@ -93,6 +93,9 @@ int prepare(Call& cl, bool count, int B, int Hq, int Hkv, int N, int Nk, int d, 
         return ATTN_ERR_UNSUPPORTED;
     if (block_kv != 64 && block_kv != 128)
         return ATTN_ERR_UNSUPPORTED;
+    // key positions plus a block stay inside int
+    if (Nk > (1 << 30))
+        return ATTN_ERR_UNSUPPORTED;
     const int64_t rows = (int64_t)B * Hq * N;
     cl.empty = rows == 0;
     cl.d = d;

@@ -316,7 +316,8 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     // l % VCPR, which holds logical chunk (l % VCPR) ^ vswz(row).  Issued at
     // the start of the block, so it travels with the K loads of the scores;
     // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
-    // Nk - 1; their P is 0.
+    // Nk - 1; their P is 0.  Lane offsets count from the block's first row, so
+    // they stay below 2^32 for any number of keys.
     // (V_RPI is a multiple of 256 / VROW and VCPR / 2 divides V_RPI / (256 /
     // VROW), so the swizzle of row i V_RPI + l / VCPR does not depend on i: a
     // block inside the cache takes one lane offset and a uniform row step)
@@ -334,7 +335,8 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
             for (int i = 0; i < V_NI; ++i) {
                 const int rv = i * V_RPI + lane / VCPR;
                 const int lc = (lane % VCPR) ^ vswz(rv);
-                g2lds(Vg, (uint32_t)min(t0 + rv, Nk - 1) * VROW + 16 * lc, vst + 1024 * i);
+                g2lds(Vg + (size_t)t0 * VROW, (uint32_t)(min(t0 + rv, Nk - 1) - t0) * VROW + 16 * lc,
+                      vst + 1024 * i);
             }
         }
     };

@@ -73,7 +73,7 @@ def fwd(A, **kw):
     (dict(causal=2), -1), (dict(order=2), -1), (dict(mode=4), -1), (dict(mode=-1), -1),
     (dict(S=0.0), -1), (dict(S=-1.0), -1), (dict(S=float("inf")), -1), (dict(S=float("nan")), -1),
     (dict(d=96), -2), (dict(d=256), -2), (dict(block_kv=32), -2), (dict(block_kv=256), -2),
-    (dict(d=0), -1),
+    (dict(d=0), -1), (dict(N=(1 << 30) + 1), -2),
     # the dynamic scale needs S = 2^k0 with 0 <= k0 <= 8; at most one ATTN_TILE_* flag;
     # no other flag bit exists
     (dict(mode=1 | 0x100, S=3.0), -1), (dict(mode=1 | 0x100, S=512.0), -1),
@@ -166,6 +166,7 @@ def test_kv_entry_points_validate(A):
                                  a.get("ws_bytes", 0), None)
     assert f(Nq=4097) == -1            # more queries than keys
     assert f(Nk=-1) == -1
+    assert f(Nk=(1 << 30) + 1) == -2   # key positions must stay well inside int
     assert f(out=None) == -1
     assert f(d=96) == -2
     assert f(Nq=0, q=None, k=None, v=None, out=None) == 0
