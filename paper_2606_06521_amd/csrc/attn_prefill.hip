@@ -170,14 +170,19 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
         else
             return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[kk], acc, 0, 0, 0);
     };
-    auto qk = [&](int j, auto whole) __attribute__((always_inline)) {
-        const int t0 = j * BC;
-        auto load_tile = [&](QFrag* dst, int kt) __attribute__((always_inline)) {
-            const uint8_t* kr = Kg + (size_t)min(t0 + 32 * kt + a_key, Nk - 1) * KROW + (QSTEP / 2) * h;
+    auto load_tile_j = [&](QFrag* dst, int j, int kt) __attribute__((always_inline)) {
+        const uint8_t* kr = Kg + (size_t)min(j * BC + 32 * kt + a_key, Nk - 1) * KROW + (QSTEP / 2) * h;
 #pragma unroll
-            for (int kk = 0; kk < DK; ++kk)
-                dst[kk] = *reinterpret_cast<const QFrag*>(kr + QSTEP * kk);
-        };
+        for (int kk = 0; kk < DK; ++kk)
+            dst[kk] = *reinterpret_cast<const QFrag*>(kr + QSTEP * kk);
+    };
+    // PHASE 2 requests the first two K tiles of a wave's first block (and its
+    // V block) before it waits for the range maxima, so that round trip
+    // overlaps the one for the maxima; qk then starts from those tiles (pre)
+    constexpr int NPRE = KT < 2 ? KT : 2;
+    auto qk = [&](int j, auto whole, auto pre) __attribute__((always_inline)) {
+        constexpr bool HAS_PRE = !std::is_same_v<decltype(pre), std::false_type>;
+        auto load_tile = [&](QFrag* dst, int kt) __attribute__((always_inline)) { load_tile_j(dst, j, kt); };
         if constexpr (decltype(whole)::value) {
             QFrag a[KT][DK];
 #pragma unroll
@@ -196,10 +201,18 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
             }
         } else {
             QFrag a[2][DK];
-            load_tile(a[0], 0);
+            if constexpr (HAS_PRE) {
+#pragma unroll
+                for (int i = 0; i < NPRE; ++i)
+#pragma unroll
+                    for (int kk = 0; kk < DK; ++kk)
+                        a[i][kk] = pre[i][kk];
+            } else {
+                load_tile(a[0], 0);
+            }
 #pragma unroll
             for (int kt = 0; kt < KT; ++kt) {
-                if (kt + 1 < KT)
+                if (kt + 1 < KT && (!HAS_PRE || kt + 1 >= NPRE))
                     load_tile(a[(kt + 1) & 1], kt + 1);
                 __builtin_amdgcn_sched_barrier(0);
                 s[kt] = mfma_qk(a[kt & 1][0], 0, f32x16{});
@@ -234,13 +247,46 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
         return halves_max(mx);
     };
 
+    uint8_t* vst = lds + w * V_BYTES;
+    auto vswz = [](int r) __attribute__((always_inline)) { return ((r / (256 / VROW)) & (VCPR / 2 - 1)) * 2; };
+    // V_j -> this wave's LDS stage, straight from HBM: round i writes LDS bytes
+    // [1024 i, +1024); lane l fills row i V_RPI + l / VCPR at physical chunk
+    // l % VCPR, which holds logical chunk (l % VCPR) ^ vswz(row).  Issued at
+    // the start of the block, so it travels with the K loads of the scores;
+    // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
+    // Nk - 1; their P is 0.  Lane offsets count from the block's first row, so
+    // they stay below 2^32 for any number of keys.
+    // (V_RPI is a multiple of 256 / VROW and VCPR / 2 divides V_RPI / (256 /
+    // VROW), so the swizzle of row i V_RPI + l / VCPR does not depend on i: a
+    // block inside the cache takes one lane offset and a uniform row step)
+    static_assert(V_RPI % (256 / VROW) == 0 && (V_RPI / (256 / VROW)) % (VCPR / 2) == 0,
+                  "the V swizzle repeats every round");
+    auto issue_v = [&](int j) __attribute__((always_inline)) {
+        const int t0 = j * BC;
+        const uint32_t v_voff = (uint32_t)((lane / VCPR) * VROW + 16 * ((lane % VCPR) ^ vswz(lane / VCPR)));
+        if (t0 + BC <= Nk) {
+#pragma unroll
+            for (int i = 0; i < V_NI; ++i)
+                g2lds(Vg + (size_t)(t0 + i * V_RPI) * VROW, v_voff, vst + 1024 * i);
+        } else {
+#pragma unroll
+            for (int i = 0; i < V_NI; ++i) {
+                const int rv = i * V_RPI + lane / VCPR;
+                const int lc = (lane % VCPR) ^ vswz(rv);
+                g2lds(Vg + (size_t)t0 * VROW, (uint32_t)(min(t0 + rv, Nk - 1) - t0) * VROW + 16 * lc,
+                      vst + 1024 * i);
+            }
+        }
+    };
+
     // ---- pass 1: row maxima over this wave's blocks ----
     float m_start = -INFINITY, m_final = -INFINITY;
+    QFrag kpre[NPRE][DK];
     if constexpr (PHASE != 2) {
         float m1 = -INFINITY;
         for (int it = it0; it < it1; ++it) {
             const int j = jof(it);
-            qk(j, std::true_type{});
+            qk(j, std::true_type{}, std::false_type{});
             mask(j);
             m1 = fmax_f(m1, row_max());
         }
@@ -270,6 +316,12 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
         for (int q = 0; q < PER; ++q) {
             const int e = tid + 64 * NW * q;
             t[q] = e < R * 32 ? mx[e] : -INFINITY;
+        }
+        if (it0 < it1) {
+            issue_v(jof(it0));
+#pragma unroll
+            for (int i = 0; i < NPRE; ++i)
+                load_tile_j(kpre[i], jof(it0), i);
         }
 #pragma unroll
         for (int q = 0; q < PER; ++q)
@@ -306,46 +358,21 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     int pv_sb = 127;
     uint32_t cnt0 = 0, cnt1 = 0, cnt2 = 0;
 
-    uint8_t* vst = lds + w * V_BYTES;
-    auto vswz = [](int r) __attribute__((always_inline)) { return ((r / (256 / VROW)) & (VCPR / 2 - 1)) * 2; };
     const int j16 = n & 15;
     const uint32_t v_lane = (uint32_t)(((j16 >> 1) + 16 * h) * VROW + (((n >> 4) | vswz(j16 >> 1)) << 4) +
                                        8 * (j16 & 1));
-    // V_j -> this wave's LDS stage, straight from HBM: round i writes LDS bytes
-    // [1024 i, +1024); lane l fills row i V_RPI + l / VCPR at physical chunk
-    // l % VCPR, which holds logical chunk (l % VCPR) ^ vswz(row).  Issued at
-    // the start of the block, so it travels with the K loads of the scores;
-    // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
-    // Nk - 1; their P is 0.  Lane offsets count from the block's first row, so
-    // they stay below 2^32 for any number of keys.
-    // (V_RPI is a multiple of 256 / VROW and VCPR / 2 divides V_RPI / (256 /
-    // VROW), so the swizzle of row i V_RPI + l / VCPR does not depend on i: a
-    // block inside the cache takes one lane offset and a uniform row step)
-    static_assert(V_RPI % (256 / VROW) == 0 && (V_RPI / (256 / VROW)) % (VCPR / 2) == 0,
-                  "the V swizzle repeats every round");
-    const uint32_t v_voff = (uint32_t)((lane / VCPR) * VROW + 16 * ((lane % VCPR) ^ vswz(lane / VCPR)));
-    auto issue_v = [&](int j) __attribute__((always_inline)) {
-        const int t0 = j * BC;
-        if (t0 + BC <= Nk) {
-#pragma unroll
-            for (int i = 0; i < V_NI; ++i)
-                g2lds(Vg + (size_t)(t0 + i * V_RPI) * VROW, v_voff, vst + 1024 * i);
-        } else {
-#pragma unroll
-            for (int i = 0; i < V_NI; ++i) {
-                const int rv = i * V_RPI + lane / VCPR;
-                const int lc = (lane % VCPR) ^ vswz(rv);
-                g2lds(Vg + (size_t)t0 * VROW, (uint32_t)(min(t0 + rv, Nk - 1) - t0) * VROW + 16 * lc,
-                      vst + 1024 * i);
-            }
-        }
-    };
 
-    for (int it = it0; it < it1; ++it) {
+    // one block of the range; PHASE 2's first block has its V and first K
+    // tiles requested already
+    auto block = [&](int it, auto first) __attribute__((always_inline)) {
         const int j = jof(it);
         const int t0 = j * BC;
-        issue_v(j);
-        qk(j, std::false_type{});
+        if constexpr (decltype(first)::value) {
+            qk(j, std::false_type{}, kpre);
+        } else {
+            issue_v(j);
+            qk(j, std::false_type{}, std::false_type{});
+        }
         mask(j);
         const float mx = row_max();
         const bool vis = mx > -INFINITY;            // the row has a key in this block
@@ -447,7 +474,16 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
             else
                 o[dt] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(av, bop, o[dt], 0, 0, 0, 0, 0, 0);
         }
+    };
+    int it = it0;
+    if constexpr (PHASE == 2) {
+        if (it < it1) {
+            block(it, std::true_type{});
+            ++it;
+        }
     }
+    for (; it < it1; ++it)
+        block(it, std::false_type{});
 
     // ---- merge: bring each wave's (O, l) to the row's final maximum and sum ----
     const float mc_final = m_final * c;
