@@ -252,8 +252,9 @@ __global__ void __launch_bounds__(64 * kPrefillWaves) prefill_kernel(Params p)
     // V_j -> this wave's LDS stage, straight from HBM: round i writes LDS bytes
     // [1024 i, +1024); lane l fills row i V_RPI + l / VCPR at physical chunk
     // l % VCPR, which holds logical chunk (l % VCPR) ^ vswz(row).  Issued at
-    // the start of the block, so it travels with the K loads of the scores;
-    // awaited (vmcnt(0)) just before P.V.  Keys past the cache end read row
+    // the start of the block (PHASE 2's first block: with the range maxima),
+    // so it travels with the K loads of the scores; awaited (vmcnt(0)) just
+    // before P.V.  Keys past the cache end read row
     // Nk - 1; their P is 0.  Lane offsets count from the block's first row, so
     // they stay below 2^32 for any number of keys.
     // (V_RPI is a multiple of 256 / VROW and VCPR / 2 divides V_RPI / (256 /
