@@ -279,6 +279,26 @@ def with_delta(inp: AttnInputs, delta: float) -> AttnInputs:
                       dict(inp.meta))
 
 
+def with_sink_cluster(inp: AttnInputs, start: int, count: int, delta: float) -> AttnInputs:
+    """A second sink cluster: keys start .. start+count-1 of every KV head get
+    the sink channel of a sink with gap ``delta`` (the same rounding as the
+    first cluster), so sinks are spread over the sequence rather than all at
+    position 0.  Q, V and every other key are unchanged.  f32 and bf16 inputs."""
+    if inp.fmt not in ("f32", "bf16_e4m3"):
+        raise ValueError("sink clusters are built for the f32 and bf16 formats")
+    if not (0 <= start and count > 0 and start + count <= inp.N):
+        raise ValueError("cluster outside the keys")
+    bf16 = inp.fmt == "bf16_e4m3"
+    val = sink_channel(1, inp.d, delta, 1, None, bf16)[0]
+    k32 = inp.k32.copy()
+    k32[:, :, start:start + count, inp.d - 1] = val
+    k_dev = _bf16_bits(k32) if bf16 else k32
+    clusters = list(inp.meta.get("sink_clusters", [])) + [(start, count, delta)]
+    return AttnInputs(inp.B, inp.Hq, inp.Hkv, inp.N, inp.d, inp.fmt, inp.delta, inp.n_sink,
+                      inp.q32, k32, inp.v32, inp.q_dev, k_dev, inp.v_dev, inp.delta_eff,
+                      dict(inp.meta, sink_clusters=clusters))
+
+
 def last_queries(inp: AttnInputs, nq: int) -> AttnInputs:
     """The KV-cache prefill shape: the same keys and values, and only the last
     ``nq`` query rows (positions N - nq .. N - 1 of the sequence)."""

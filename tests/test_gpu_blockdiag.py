@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import oracle
-from paper_2606_06521_amd.inputs import make_inputs
+from paper_2606_06521_amd.inputs import make_inputs, with_sink_cluster
 from paper_2606_06521_amd.workloads import WORKLOADS
 from tests.gpu_helpers import log, to_device
 
@@ -46,6 +46,26 @@ def test_small_exact(mode, tile, d, bkv):
         assert np.array_equal(hist, o_hist), label
         assert np.array_equal(bz, o_bz), label
         assert np.array_equal(cnt.reshape(-1, 3), o_cnt), label
+
+
+@pytest.mark.parametrize("mode,tile", [("faithful", None), ("fast", 256), ("fast", 128)])
+def test_multi_sink_exact(mode, tile):
+    # sinks spread over the sequence: gap 8 at keys 0-3, gap 30 at keys
+    # 160-163, gap 12 at keys 700-703 (blocks 0, 2 and 10 of 64; 5 and 2 of 128)
+    for d, bkv in ((64, 64), (128, 128)):
+        inp = make_inputs(1, 4, 2, 777, d, fmt=FMT[mode], delta=8.0, seed=802 + d)
+        inp = with_sink_cluster(with_sink_cluster(inp, 160, 4, 30.0), 700, 4, 12.0)
+        dev = to_device(inp)
+        for causal, order in itertools.product([False, True], ["forward", "reverse"]):
+            label = f"diag multi-sink {mode} d={d} bkv={bkv} causal={causal} {order} tile={tile}"
+            log(label)
+            hist, bz, cnt = _run(dev, mode, 256.0, order, causal, bkv, tile=tile)
+            _, _, o_cnt, o_hist, o_bz = oracle.block_diag(inp.q32, inp.k32, inp.v32, S=256.0,
+                                                          order=order, block_kv=bkv,
+                                                          causal=causal, nbins=32)
+            assert np.array_equal(hist, o_hist), label
+            assert np.array_equal(bz, o_bz), label
+            assert np.array_equal(cnt.reshape(-1, 3), o_cnt), label
 
 
 def test_sweep_head_exact():

@@ -16,7 +16,7 @@ import numpy as np
 import pytest
 
 import oracle
-from paper_2606_06521_amd.inputs import make_inputs
+from paper_2606_06521_amd.inputs import make_inputs, with_sink_cluster
 
 NB = 32
 
@@ -99,6 +99,56 @@ def test_blocks_far_below_the_maximum_are_zeroed_whole():
     _, _, _, _, bz0 = oracle.block_diag(inp.q32, inp.k32, inp.v32, S=256.0, order="forward",
                                         block_kv=Bc, cast=False, nbins=NB)
     assert bz0.sum() == 0
+
+
+def test_multi_sink_blocks_follow_their_own_gap():
+    # Sinks spread over the sequence (Limitations and Future Work): keys 0-3
+    # carry a gap of 8 and keys 160-163 (block 2 of 64) a gap of 30.  With the
+    # single gap replaced by each block's gap below the running maximum,
+    # Prop. 1 says which blocks lose every code (gap >= 10 + log2 256 = 18 in
+    # log2 units, i.e. >= 12.5 in logits), and Theorem 2 which lose none:
+    #   forward: blocks 3-7 follow the big cluster and are ~26 below it;
+    #   reverse: blocks 7-3 come first (Gaussian scores only: no zeros),
+    #            blocks 1 and 0 (the small sinks included) come after it;
+    #   both:    block 2 keeps exactly its four cluster codes.
+    N, Bc, d, NB = 512, 64, 64, 32
+    inp = with_sink_cluster(make_inputs(1, 2, 1, N, d, fmt="f32", delta=8.0, seed=75),
+                            160, 4, 30.0)
+    full, keep = N * Bc, N * (Bc - 4)
+    for order, zeroed, clean, before in (("forward", [3, 4, 5, 6, 7], [], [0, 1]),
+                                         ("reverse", [0, 1], [3, 4, 5, 6, 7], [3, 4, 5, 6, 7])):
+        _, _, _, hist, bz = oracle.block_diag(inp.q32, inp.k32, inp.v32, S=256.0, order=order,
+                                              block_kv=Bc, causal=False, nbins=NB)
+        for j in zeroed:
+            assert np.all(bz[0, :, j] == full), (order, j)
+            assert np.all(hist[0, :, j, :18] == 0), (order, j)     # every row's gap >= 18
+        for j in clean:
+            assert np.all(bz[0, :, j] == 0), (order, j)
+        for j in before:       # measured against the running maximum, not the final one
+            assert np.all(hist[0, :, j, 18:] == 0), (order, j)
+        assert np.all(bz[0, :, 2] == keep), order
+        # the cluster's block is its own maximum: gap 0 for every row that has
+        # not seen a larger one, which in both orders is every row
+        assert np.all(hist[0, :, 2, 0] == N), order
+
+
+def test_sink_cluster_inputs():
+    # the generator's second cluster: only the cluster keys' sink channel
+    # changes, to the first cluster's value for the same gap, in both formats
+    for fmt in ("f32", "bf16_e4m3"):
+        base = make_inputs(1, 2, 1, 300, 64, fmt=fmt, delta=8.0, seed=76)
+        two = with_sink_cluster(base, 100, 4, 8.0)
+        diff = np.argwhere(two.k32 != base.k32)
+        assert set(map(tuple, diff[:, 2:])) <= {(t, 63) for t in range(100, 104)}
+        assert np.all(two.k32[:, :, 100:104, 63] == base.k32[:, :, 0:4, 63])
+        if fmt == "bf16_e4m3":
+            dec = (two.k_dev.astype(np.uint32) << 16).view(np.float32)
+            assert np.array_equal(dec, two.k32)
+        assert np.array_equal(two.q32, base.q32) and np.array_equal(two.v32, base.v32)
+    with pytest.raises(ValueError):
+        with_sink_cluster(make_inputs(1, 1, 1, 64, 64, fmt="e4m3", delta=8.0, seed=77), 8, 4, 8.0)
+    with pytest.raises(ValueError):
+        with_sink_cluster(base, 298, 4, 8.0)
 
 
 def test_rejects_bad_bins():
