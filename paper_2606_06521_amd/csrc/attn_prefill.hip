@@ -630,6 +630,21 @@ __global__ void __launch_bounds__(128) prefill_merge(Params p)
             lp[cc] = base[cc * PART + 32 * D + rr];
         }
     }
+    // the tile's final maximum (for lse): the row's PIECES threads each take
+    // up to MPT of the C * NW range maxima, requested with the partial sums,
+    // and then the maximum across the group (exact in any order)
+    constexpr int NW = kPrefillWaves;
+    constexpr int MPT = (8 * NW + PIECES - 1) / PIECES;
+    float mloc = -INFINITY;
+    if (p.lse) {
+        const float* mx = p.ws_max + (size_t)unit * C * NW * 32 + rr;
+#pragma unroll
+        for (int i = 0; i < MPT; ++i) {
+            const int e = piece + PIECES * i;
+            if (e < C * NW)
+                mloc = fmax_f(mloc, mx[32 * e]);
+        }
+    }
     f32x4 acc = part[0];
     float l = lp[0];
 #pragma unroll
@@ -652,20 +667,13 @@ __global__ void __launch_bounds__(128) prefill_merge(Params p)
         v4[3] = acc[3] * inv;
         *reinterpret_cast<f32x4*>(p.out + flat * D + 4 * piece) = v4;
     }
-    if (piece == 0 && p.lse) {
-        constexpr int NW = kPrefillWaves;
-        float mf = -INFINITY;
-        const float* mx = p.ws_max + (size_t)unit * C * NW * 32 + rr;
-        for (int cc = 0; cc < C; ++cc) {
-            float t[NW];
+    // (a row's threads all return above, or none do: the group is whole here)
+    if (p.lse) {
 #pragma unroll
-            for (int v = 0; v < NW; ++v)
-                t[v] = mx[32 * (cc * NW + v)];
-#pragma unroll
-            for (int v = 0; v < NW; ++v)
-                mf = fmax_f(mf, t[v]);
-        }
-        p.lse[flat] = (mf * p.c + __builtin_log2f(l)) * 0.6931471805599453f;
+        for (int off = PIECES / 2; off > 0; off >>= 1)
+            mloc = fmax_f(mloc, __shfl_xor(mloc, off, 64));
+        if (piece == 0)
+            p.lse[flat] = (mloc * p.c + __builtin_log2f(l)) * 0.6931471805599453f;
     }
 }
 
